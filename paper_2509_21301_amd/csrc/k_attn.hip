@@ -1,0 +1,279 @@
+// Flash-style attention for vision encode (bidirectional) and LLM prefill (causal, grouped-query).
+//
+// softmax(q k^T / sqrt(d)) v is computed tile by tile with an online softmax in fp32 (the
+// attention kernel of the paper's Table 3; the paper used FlashInfer, Sec. 4).  gfx950 design:
+//  * a workgroup owns 128 queries of one head (4 waves x 32); K and V^T tiles of 64 keys are
+//    staged in LDS and shared by the 4 waves; the next tile is prefetched into registers while
+//    the current one is consumed;
+//  * S^T = K Q^T with MFMA 32x32x16 so that each lane owns ONE query (column) and 16 keys:
+//    the row max / row sum need a single cross-lane exchange (lane ^ 32), and the output
+//    rescale is per lane;
+//  * O^T = V^T P^T with the same MFMA: the probabilities already sit in the B-operand layout,
+//    because an MFMA fragment's k index only has to agree between its A and B operands;
+//    V is therefore stored transposed by the projection kernel;
+//  * head_dim 64 / 80 / 128 (80 = 5 k-steps of 16 for QK^T; PV pads the output rows to 96);
+//  * fp32 mode (tiny-stack exact mode): q, k, v, p are split into bf16 hi + lo parts and the
+//    three significant cross products are accumulated.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace nova {
+
+constexpr int AQ = 128;   // queries per workgroup
+constexpr int AK = 64;    // keys per tile
+
+template <typename T, int D, bool CAUSAL>
+__global__ void __launch_bounds__(256) attn_kernel(AttnArgs p) {
+  constexpr bool F32 = sizeof(T) == 4;
+  constexpr int NS = D / 16;                // k-steps of QK^T
+  constexpr int DP = (D + 31) / 32 * 32;    // output rows padded to 32
+  constexpr int NC = DP / 32;               // output row blocks
+  constexpr int KP = D + 8;                 // LDS pitch of K rows (bf16)
+  constexpr int VP = AK + 4;                // LDS pitch of V^T rows (bf16)
+  constexpr int NPART = F32 ? 2 : 1;
+  __shared__ __align__(16) bf16_t ks[NPART][AK * KP];
+  __shared__ __align__(16) bf16_t vs[NPART][DP * VP];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, lq = lane & 31;
+  const int nqb = (p.sq + AQ - 1) / AQ;
+  const int qb = CAUSAL ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;   // heavy causal blocks first
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int kvh = h / (p.n_q / p.n_kv);
+  const int q0 = qb * AQ;
+  const int qrow = q0 + wave * 32 + lq;
+
+  const T* Q = reinterpret_cast<const T*>(p.q) + (size_t)b * p.q_batch + (size_t)h * D;
+  const T* K = reinterpret_cast<const T*>(p.k) + (size_t)b * p.k_batch + (size_t)kvh * D;
+  const T* VT = reinterpret_cast<const T*>(p.vt) + ((size_t)b * p.n_kv + kvh) * D * (size_t)p.sk_pad;
+
+  // ---- Q fragments (B operand of S^T = K Q^T): query lq, dims 16s + 8g .. +8
+  Frag8 qh[NS], ql[F32 ? NS : 1];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    if (qrow < p.sq) {
+      const T* src = Q + (size_t)qrow * p.q_row + 16 * s + 8 * g;
+      if constexpr (F32) {
+        float x[8];
+        *reinterpret_cast<float4*>(x) = *reinterpret_cast<const float4*>(src);
+        *reinterpret_cast<float4*>(x + 4) = *reinterpret_cast<const float4*>(src + 4);
+        split8(x, qh[s], ql[s]);
+      } else {
+        qh[s] = *reinterpret_cast<const Frag8*>(src);
+      }
+    } else {
+      qh[s] = zero_frag();
+      if constexpr (F32) ql[s] = zero_frag();
+    }
+  }
+
+  // ---- tile staging (global -> registers -> LDS)
+  constexpr int EPC = F32 ? 4 : 8;                     // elements per 16-byte chunk
+  constexpr int K_CH = AK * D / EPC;
+  constexpr int V_CH = D * AK / EPC;
+  constexpr int K_IT = (K_CH + 255) / 256, V_IT = (V_CH + 255) / 256;
+  u32x4 rk[K_IT], rv[V_IT];
+  auto load_tile = [&](int kv0) {
+#pragma unroll
+    for (int i = 0; i < K_IT; ++i) {
+      const int c = tid + i * 256;
+      rk[i] = u32x4{0u, 0u, 0u, 0u};
+      if (c < K_CH) {
+        const int r = c / (D / EPC), col = (c % (D / EPC)) * EPC;
+        if (kv0 + r < p.sk) rk[i] = *reinterpret_cast<const u32x4*>(K + (size_t)(kv0 + r) * p.k_row + col);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < V_IT; ++i) {
+      const int c = tid + i * 256;
+      if (c < V_CH) {
+        const int r = c / (AK / EPC), col = (c % (AK / EPC)) * EPC;
+        rv[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)r * p.sk_pad + kv0 + col);
+      }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < K_IT; ++i) {
+      const int c = tid + i * 256;
+      if (c < K_CH) {
+        const int r = c / (D / EPC), col = (c % (D / EPC)) * EPC;
+        if constexpr (F32) {
+          float x[4] = {__uint_as_float(rk[i][0]), __uint_as_float(rk[i][1]), __uint_as_float(rk[i][2]), __uint_as_float(rk[i][3])};
+          bf16_t hh[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) hh[j] = f2bf(x[j]);
+          *reinterpret_cast<uint2*>(&ks[0][r * KP + col]) =
+              make_uint2((uint32_t)hh[0] | ((uint32_t)hh[1] << 16), (uint32_t)hh[2] | ((uint32_t)hh[3] << 16));
+          *reinterpret_cast<uint2*>(&ks[1][r * KP + col]) =
+              make_uint2(pack2(x[0] - bf2f(hh[0]), x[1] - bf2f(hh[1])), pack2(x[2] - bf2f(hh[2]), x[3] - bf2f(hh[3])));
+        } else {
+          *reinterpret_cast<u32x4*>(&ks[0][r * KP + col]) = rk[i];
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < V_IT; ++i) {
+      const int c = tid + i * 256;
+      if (c < V_CH) {
+        const int r = c / (AK / EPC), col = (c % (AK / EPC)) * EPC;
+        if constexpr (F32) {
+          float x[4] = {__uint_as_float(rv[i][0]), __uint_as_float(rv[i][1]), __uint_as_float(rv[i][2]), __uint_as_float(rv[i][3])};
+          bf16_t hh[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) hh[j] = f2bf(x[j]);
+          *reinterpret_cast<uint2*>(&vs[0][r * VP + col]) =
+              make_uint2((uint32_t)hh[0] | ((uint32_t)hh[1] << 16), (uint32_t)hh[2] | ((uint32_t)hh[3] << 16));
+          *reinterpret_cast<uint2*>(&vs[1][r * VP + col]) =
+              make_uint2(pack2(x[0] - bf2f(hh[0]), x[1] - bf2f(hh[1])), pack2(x[2] - bf2f(hh[2]), x[3] - bf2f(hh[3])));
+        } else {
+          *reinterpret_cast<uint2*>(&vs[0][r * VP + col]) = make_uint2(rv[i][0], rv[i][1]);
+          *reinterpret_cast<uint2*>(&vs[0][r * VP + col + 4]) = make_uint2(rv[i][2], rv[i][3]);
+        }
+      }
+    }
+  };
+
+  f32x16 o[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) o[c] = f32x16{};
+  float m_run = -1e30f, l_run = 0.f;
+  const float scale = 1.4426950408889634f / sqrtf((float)D);
+
+  const int kv_end = CAUSAL ? min(p.sk, q0 + AQ) : p.sk;
+  const int wave_qmax = q0 + wave * 32 + 31;
+  load_tile(0);
+  for (int kv0 = 0; kv0 < kv_end; kv0 += AK) {
+    __syncthreads();          // previous tile fully consumed
+    store_tile();
+    __syncthreads();
+    if (kv0 + AK < kv_end) load_tile(kv0 + AK);
+    if (CAUSAL && kv0 > wave_qmax) continue;   // every key of this tile is in this wave's future
+
+    // S^T = K Q^T for two 32-key blocks
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      sacc[kb] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const int off = (kb * 32 + lq) * KP + 16 * s + 8 * g;
+        Frag8 ka = *reinterpret_cast<const Frag8*>(&ks[0][off]);
+        sacc[kb] = mfma32(ka, qh[s], sacc[kb]);
+        if constexpr (F32) {
+          Frag8 kl = *reinterpret_cast<const Frag8*>(&ks[1][off]);
+          sacc[kb] = mfma32(kl, qh[s], sacc[kb]);
+          sacc[kb] = mfma32(ka, ql[s], sacc[kb]);
+        }
+      }
+    }
+    // online softmax for query qrow: keys kv0 + 32kb + 8(r/4) + 4g + r%4
+    float tmax = -1e30f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kidx = kv0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        const bool ok = kidx < p.sk && (!CAUSAL || kidx <= qrow);
+        const float sv = ok ? sacc[kb][r] * scale : -INFINITY;
+        sacc[kb][r] = sv;
+        tmax = fmaxf(tmax, sv);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    const float corr = exp2f(m_run - m_new);
+    float rsum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pv = exp2f(sacc[kb][r] - m_new);
+        sacc[kb][r] = pv;
+        rsum += pv;
+      }
+    rsum += __shfl_xor(rsum, 32, 64);
+    l_run = l_run * corr + rsum;
+    m_run = m_new;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[c][r] *= corr;
+
+    // O^T += V^T P^T, 16 keys per MFMA
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        Frag8 ph, pl;
+        if constexpr (F32) {
+          float x[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] = sacc[kb][8 * t + e];
+          split8(x, ph, pl);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) ph.w[e] = pack2(sacc[kb][8 * t + 2 * e], sacc[kb][8 * t + 2 * e + 1]);
+        }
+        const int key = kb * 32 + 16 * t + 4 * g;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const int vrow = c * 32 + lq;
+          Frag8 va;
+          const uint2 lo = *reinterpret_cast<const uint2*>(&vs[0][vrow * VP + key]);
+          const uint2 hi = *reinterpret_cast<const uint2*>(&vs[0][vrow * VP + key + 8]);
+          va.w[0] = lo.x; va.w[1] = lo.y; va.w[2] = hi.x; va.w[3] = hi.y;
+          o[c] = mfma32(va, ph, o[c]);
+          if constexpr (F32) {
+            Frag8 vl;
+            const uint2 lo2 = *reinterpret_cast<const uint2*>(&vs[1][vrow * VP + key]);
+            const uint2 hi2 = *reinterpret_cast<const uint2*>(&vs[1][vrow * VP + key + 8]);
+            vl.w[0] = lo2.x; vl.w[1] = lo2.y; vl.w[2] = hi2.x; vl.w[3] = hi2.y;
+            o[c] = mfma32(vl, ph, o[c]);
+            o[c] = mfma32(va, pl, o[c]);
+          }
+        }
+      }
+  }
+
+  if (qrow >= p.sq) return;
+  const float inv = 1.0f / l_run;
+  T* out = reinterpret_cast<T*>(p.out) + (size_t)b * p.o_batch + (size_t)qrow * p.o_row + (size_t)h * D;
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int col = c * 32 + 8 * r4 + 4 * g;
+      if (col >= D) continue;
+      if constexpr (F32) {
+        *reinterpret_cast<float4*>(out + col) =
+            make_float4(o[c][4 * r4] * inv, o[c][4 * r4 + 1] * inv, o[c][4 * r4 + 2] * inv, o[c][4 * r4 + 3] * inv);
+      } else {
+        *reinterpret_cast<uint2*>(out + col) =
+            make_uint2(pack2(o[c][4 * r4] * inv, o[c][4 * r4 + 1] * inv), pack2(o[c][4 * r4 + 2] * inv, o[c][4 * r4 + 3] * inv));
+      }
+    }
+}
+
+template <typename T, int D>
+static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
+  dim3 grid((p.sq + AQ - 1) / AQ, p.n_q, p.batch);
+  if (p.causal) hipLaunchKernelGGL((attn_kernel<T, D, true>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((attn_kernel<T, D, false>), grid, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t attention(const AttnArgs& p, int head_dim, hipStream_t s) {
+  if (p.sq <= 0 || p.sk <= 0) return hipSuccess;
+  if (p.n_kv <= 0 || p.n_q % p.n_kv || p.sk_pad % AK || p.sk_pad < p.sk) return hipErrorInvalidValue;
+  switch (head_dim) {
+    case 64: return attn_launch<T, 64>(p, s);
+    case 80: return attn_launch<T, 80>(p, s);
+    case 128: return attn_launch<T, 128>(p, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template hipError_t attention<bf16_t>(const AttnArgs&, int, hipStream_t);
+template hipError_t attention<float>(const AttnArgs&, int, hipStream_t);
+
+}  // namespace nova

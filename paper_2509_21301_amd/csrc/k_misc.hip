@@ -1,0 +1,298 @@
+// Memory-bound glue kernels of the three stages: LayerNorm/RMSNorm (with the 2x2 patch-merge
+// scatter fused into the LayerNorm store), patchify, QKV split with rotary embedding, transposed
+// V and paged-cache writes, embedding gather and greedy argmax.  All use 16-byte coalesced
+// accesses along the hidden dimension; statistics are accumulated in fp32.
+#include <algorithm>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace nova {
+
+// ------------------------------------------------------------------ norms (one wave per row)
+template <typename T>
+__global__ void norm_kernel(const float* __restrict__ x, int M, int H, const bf16_t* __restrict__ g,
+                            const bf16_t* __restrict__ bb, float eps, int ln, T* __restrict__ out, int ldo,
+                            int merge, int gh, int gw) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)row * H);
+  const int n4 = H / 4;
+  float s = 0.f, ss = 0.f;
+  for (int i = lane; i < n4; i += 64) {
+    float4 v = xr[i];
+    s += v.x + v.y + v.z + v.w;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  s = wave_sum(s);
+  float mean = 0.f, rstd;
+  if (ln) {
+    mean = s / H;
+    float vs = 0.f;   // second pass for a well-conditioned variance
+    for (int i = lane; i < n4; i += 64) {
+      float4 v = xr[i];
+      float a = v.x - mean, b = v.y - mean, c = v.z - mean, d = v.w - mean;
+      vs += a * a + b * b + c * c + d * d;
+    }
+    rstd = rsqrtf(wave_sum(vs) / H + eps);
+  } else {
+    rstd = rsqrtf(wave_sum(ss) / H + eps);
+  }
+  size_t orow = row, ocol = 0;
+  if (merge > 1) {
+    const int per_img = gh * gw;
+    const int img = row / per_img, r = row % per_img, py = r / gw, px = r % gw;
+    orow = (size_t)img * (per_img / (merge * merge)) + (py / merge) * (gw / merge) + px / merge;
+    ocol = (size_t)((py % merge) * merge + px % merge) * H;
+  }
+  T* o = out + orow * ldo + ocol;
+  for (int i = lane; i < n4; i += 64) {
+    float4 v = xr[i];
+    float y[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = 4 * i + j;
+      float t = (y[j] - mean) * rstd * bf2f(g[c]);
+      if (ln) t += bf2f(bb[c]);
+      o[c] = from_f<T>(t);
+    }
+  }
+}
+
+template <typename T>
+hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln, T* out,
+                     int ldo, int merge, int gh, int gw, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (H % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((norm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, g, b, eps, ln, out, ldo, merge, gh, gw);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ patchify
+template <typename T>
+__global__ void patchify_kernel(const bf16_t* __restrict__ img, int B, int H, int W, int p, int kpad, T* __restrict__ out) {
+  const int gw = W / p, gh = H / p;
+  const long total = (long)B * gh * gw * kpad;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int col = (int)(idx % kpad);
+    const long prow = idx / kpad;
+    float v = 0.f;
+    if (col < 3 * p * p) {
+      const int c = col % 3, px = (col / 3) % p, py = col / (3 * p);
+      const int img_i = (int)(prow / (gh * gw)), r = (int)(prow % (gh * gw));
+      const int y = (r / gw) * p + py, x = (r % gw) * p + px;
+      v = bf2f(img[(((size_t)img_i * H + y) * W + x) * 3 + c]);
+    }
+    out[idx] = from_f<T>(v);
+  }
+}
+
+template <typename T>
+hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* out, hipStream_t s) {
+  const long total = (long)B * (H / p) * (W / p) * kpad;
+  if (total <= 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL((patchify_kernel<T>), dim3(grid), dim3(256), 0, s, img, B, H, W, p, kpad, out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ rotary embedding in place
+// Half-split pairing: (c, c + D/2) rotate by angle pos * theta^(-2c/D).
+template <typename T>
+__global__ void rope_inplace_kernel(T* __restrict__ qkv, int rows, int S, int n_rot_heads, int D, float theta, int pos0, int ld) {
+  const int half = D / 2;
+  const long total = (long)rows * n_rot_heads * half;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % half);
+    const long t = idx / half;
+    const int hh = (int)(t % n_rot_heads);
+    const int row = (int)(t / n_rot_heads);
+    float sn, cs;
+    rope_sincos(pos0 + row % S, c, D, theta, &sn, &cs);
+    T* e = qkv + (size_t)row * ld + (size_t)hh * D;
+    const float x1 = to_f<T>(e[c]), x2 = to_f<T>(e[c + half]);
+    e[c] = from_f<T>(x1 * cs - x2 * sn);
+    e[c + half] = from_f<T>(x2 * cs + x1 * sn);
+  }
+}
+
+// V transpose for attention (and the paged K/V cache writes): one workgroup per
+// (64-token tile, kv head, batch).  V rows go through LDS so that V^T rows are written whole.
+template <typename T>
+__global__ void __launch_bounds__(256) kv_scatter_kernel(const T* __restrict__ qkv, int S, int n_q, int n_kv, int D,
+                                                        T* __restrict__ vt, int sk_pad, T* __restrict__ kpool,
+                                                        T* __restrict__ vpool, const int* __restrict__ table, int block) {
+  __shared__ float tile[64][129];
+  const int t0 = blockIdx.x * 64, kvh = blockIdx.y, b = blockIdx.z;
+  const int ld = (n_q + 2 * n_kv) * D;
+  const T* vsrc = qkv + (size_t)b * S * ld + (size_t)(n_q + n_kv) * D + (size_t)kvh * D;
+  const T* ksrc = qkv + (size_t)b * S * ld + (size_t)n_q * D + (size_t)kvh * D;
+  for (int i = threadIdx.x; i < 64 * D; i += 256) {
+    const int t = i / D, c = i % D;
+    tile[t][c] = (t0 + t < S) ? to_f<T>(vsrc[(size_t)(t0 + t) * ld + c]) : 0.f;
+  }
+  __syncthreads();
+  // V^T [b][kvh][D][sk_pad]; keys beyond S are zero
+  T* vdst = vt + ((size_t)b * n_kv + kvh) * D * (size_t)sk_pad;
+  for (int i = threadIdx.x; i < 64 * D; i += 256) {
+    const int c = i / 64, t = i % 64;
+    if (t0 + t < sk_pad) vdst[(size_t)c * sk_pad + t0 + t] = from_f<T>(tile[t][c]);
+  }
+  if (table == nullptr) return;
+  // paged cache: K [blk][kvh][slot][D], V [blk][kvh][D][slot]
+  for (int i = threadIdx.x; i < 64 * D; i += 256) {
+    const int t = i / D, c = i % D;
+    const int tok = t0 + t;
+    if (tok >= S) continue;
+    const int phys = table[tok / block], slot = tok % block;
+    kpool[(((size_t)phys * n_kv + kvh) * block + slot) * D + c] = ksrc[(size_t)tok * ld + c];
+  }
+  for (int i = threadIdx.x; i < 64 * D; i += 256) {
+    const int c = i / 64, t = i % 64;
+    const int tok = t0 + t;
+    if (tok >= S) continue;
+    const int phys = table[tok / block], slot = tok % block;
+    vpool[(((size_t)phys * n_kv + kvh) * D + c) * block + slot] = from_f<T>(tile[t][c]);
+  }
+}
+
+template <typename T>
+hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0, T* vt,
+                       int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s) {
+  if (S <= 0) return hipSuccess;
+  if (D > 128 || sk_pad < S) return hipErrorInvalidValue;
+  const int ld = (n_q + 2 * n_kv) * D;
+  if (rope_theta > 0.f) {
+    const long total = (long)batch * S * (n_q + n_kv) * (D / 2);
+    const int grid = (int)std::min<long>((total + 255) / 256, 65536);
+    hipLaunchKernelGGL((rope_inplace_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, batch * S, S, n_q + n_kv, D,
+                       rope_theta, pos0, ld);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  dim3 grid((sk_pad + 63) / 64, n_kv, batch);
+  hipLaunchKernelGGL((kv_scatter_kernel<T>), grid, dim3(256), 0, s, qkv, S, n_q, n_kv, D, vt, sk_pad, kpool, vpool,
+                     table, block);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ decode QKV: rotate, store q, append k/v
+template <typename T>
+__global__ void qkv_decode_kernel(const float* __restrict__ qkv, int B, int n_q, int n_kv, int D, float theta,
+                                  const int* __restrict__ pos, T* __restrict__ qout, T* __restrict__ kpool,
+                                  T* __restrict__ vpool, const int* __restrict__ tables, int max_blocks, int block) {
+  const int half = D / 2;
+  const int heads = n_q + 2 * n_kv;
+  const long total = (long)B * heads * half;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % half);
+    const int hh = (int)((idx / half) % heads);
+    const int b = (int)(idx / ((long)half * heads));
+    const int ps = pos[b];
+    const float* e = qkv + (size_t)b * heads * D + (size_t)hh * D;
+    float x1 = e[c], x2 = e[c + half];
+    if (hh < n_q + n_kv) {
+      float sn, cs;
+      rope_sincos(ps, c, D, theta, &sn, &cs);
+      const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
+      x1 = y1; x2 = y2;
+    }
+    if (hh < n_q) {
+      T* q = qout + ((size_t)b * n_q + hh) * D;
+      q[c] = from_f<T>(x1);
+      q[c + half] = from_f<T>(x2);
+      continue;
+    }
+    const int phys = tables[(size_t)b * max_blocks + ps / block], slot = ps % block;
+    if (hh < n_q + n_kv) {
+      const int kvh = hh - n_q;
+      T* k = kpool + (((size_t)phys * n_kv + kvh) * block + slot) * D;
+      k[c] = from_f<T>(x1);
+      k[c + half] = from_f<T>(x2);
+    } else {
+      const int kvh = hh - n_q - n_kv;
+      T* v = vpool + ((size_t)phys * n_kv + kvh) * D * block;
+      v[(size_t)c * block + slot] = from_f<T>(x1);
+      v[(size_t)(c + half) * block + slot] = from_f<T>(x2);
+    }
+  }
+}
+
+template <typename T>
+hipError_t qkv_decode(const float* qkv, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos, T* qout,
+                      T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  const long total = (long)B * (n_q + 2 * n_kv) * (D / 2);
+  const int grid = (int)std::min<long>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL((qkv_decode_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, B, n_q, n_kv, D, rope_theta, pos, qout,
+                     kpool, vpool, tables, max_blocks, block);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ embedding gather
+template <typename T>
+__global__ void embed_kernel(const T* __restrict__ vis, int n_vis, const int* __restrict__ ids, int n_ids,
+                             const bf16_t* __restrict__ embed, int H, float* __restrict__ x) {
+  const long total = (long)(n_vis + n_ids) * H;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int r = (int)(idx / H), c = (int)(idx % H);
+    x[idx] = r < n_vis ? to_f<T>(vis[(size_t)r * H + c]) : bf2f(embed[(size_t)ids[r - n_vis] * H + c]);
+  }
+}
+
+template <typename T>
+hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const bf16_t* embed, int H, float* x,
+                      hipStream_t s) {
+  const long total = (long)(n_vis + n_ids) * H;
+  if (total <= 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL((embed_kernel<T>), dim3(grid), dim3(256), 0, s, vis, n_vis, ids, n_ids, embed, H, x);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ greedy argmax (ties -> lowest index)
+__global__ void argmax_kernel(const float* __restrict__ logits, int V, int* __restrict__ out) {
+  const float* row = logits + (size_t)blockIdx.x * V;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int i = threadIdx.x; i < V; i += blockDim.x) {
+    const float v = row[i];
+    if (v > best) { best = v; bi = i; }   // strided scan: first hit per thread is its lowest index
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float ov = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
+  }
+  __shared__ float sv[16];
+  __shared__ int si[16];
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { sv[w] = best; si[w] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int j = 1; j < (int)(blockDim.x >> 6); ++j)
+      if (sv[j] > best || (sv[j] == best && si[j] < bi)) { best = sv[j]; bi = si[j]; }
+    out[blockIdx.x] = bi;
+  }
+}
+
+hipError_t argmax_rows(const float* logits, int B, int V, int* out, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_kernel, dim3(B), dim3(1024), 0, s, logits, V, out);
+  return hipGetLastError();
+}
+
+template hipError_t norm_rows<bf16_t>(const float*, int, int, const bf16_t*, const bf16_t*, float, int, bf16_t*, int, int, int, int, hipStream_t);
+template hipError_t norm_rows<float>(const float*, int, int, const bf16_t*, const bf16_t*, float, int, float*, int, int, int, int, hipStream_t);
+template hipError_t patchify<bf16_t>(const bf16_t*, int, int, int, int, int, bf16_t*, hipStream_t);
+template hipError_t patchify<float>(const bf16_t*, int, int, int, int, int, float*, hipStream_t);
+template hipError_t qkv_prefill<bf16_t>(bf16_t*, int, int, int, int, int, float, int, bf16_t*, int, bf16_t*, bf16_t*, const int*, int, hipStream_t);
+template hipError_t qkv_prefill<float>(float*, int, int, int, int, int, float, int, float*, int, float*, float*, const int*, int, hipStream_t);
+template hipError_t qkv_decode<bf16_t>(const float*, int, int, int, int, float, const int*, bf16_t*, bf16_t*, bf16_t*, const int*, int, int, hipStream_t);
+template hipError_t qkv_decode<float>(const float*, int, int, int, int, float, const int*, float*, float*, float*, const int*, int, int, hipStream_t);
+template hipError_t embed_rows<bf16_t>(const bf16_t*, int, const int*, int, const bf16_t*, int, float*, hipStream_t);
+template hipError_t embed_rows<float>(const float*, int, const int*, int, const bf16_t*, int, float*, hipStream_t);
+
+}  // namespace nova

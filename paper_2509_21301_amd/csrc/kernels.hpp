@@ -1,0 +1,102 @@
+// Host-side launchers of the gfx950 kernels (internal to libnova; the public C ABI is in nova.h).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <type_traits>
+
+#ifndef NOVA_BF16_T
+#define NOVA_BF16_T
+typedef uint16_t bf16_t;
+#endif
+
+namespace nova {
+
+enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_POS = 3, EPI_SWIGLU = 4 };
+
+// C[M,N] = A[M,K] W[N,K]^T (+bias) with epilogue.  A has element type TA, row stride lda.
+// STORE/GELU/SWIGLU write OT into out (row stride ldo); RESID adds into the fp32 out;
+// POS writes fp32 out = acc + bias + pos[m % pos_rows] (pos is bf16 [pos_rows, N]).
+struct GemmArgs {
+  const void* A; int lda;
+  const bf16_t* W; int ldw;
+  int M, N, K;
+  const bf16_t* bias;
+  void* out; int ldo;
+  const bf16_t* pos; int pos_rows;
+};
+template <typename TA, typename OT>
+hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s);
+
+// Thin GEMM for decode (M = B <= 32 rows): weights streamed once, split over K if needed.
+// out gets epilogue epi (STORE: OT [B, ldo]; RESID: fp32 += ; SWIGLU: OT [B, N/2]).
+// partial is fp32 workspace of gemv_partial_floats() floats.
+struct GemvArgs {
+  const void* X; int ldx;
+  const bf16_t* W; int ldw;
+  int B, N, K;
+  void* out; int ldo;
+  float* partial;
+};
+int gemv_splits(int N, int K);
+size_t gemv_partial_floats(int B, int N, int K);
+template <typename TX, typename OT>
+hipError_t gemv(const GemvArgs& p, int epi, hipStream_t s);
+
+// Flash attention (bidirectional or causal, grouped-query) for encode and prefill.
+// q, k: rows of the packed projection output; element (token t, head h, dim c) at
+//   base + t * row_stride + h * D + c  (per-batch offset batch_stride).
+// vt: V transposed, [batch][n_kv][D][sk_pad] (keys >= sk zero-filled up to sk_pad, a multiple of 64).
+// out: [batch * sq, n_q * D] rows.
+struct AttnArgs {
+  const void* q; long q_row, q_batch;
+  const void* k; long k_row, k_batch;
+  const void* vt; int sk_pad;
+  void* out; long o_row, o_batch;
+  int sq, sk, n_q, n_kv, batch;
+  int causal;
+};
+template <typename T>
+hipError_t attention(const AttnArgs& p, int head_dim, hipStream_t s);
+
+// Paged decode attention: one query per sequence against its paged KV blocks.
+struct DecAttnArgs {
+  const void* q;              // [B, n_q, D]
+  const void* kpool;          // [num_blocks, n_kv, block, D] for this layer
+  const void* vpool;
+  const int* tables; int max_blocks;
+  const int* pos;             // query position; context = pos + 1
+  void* out;                  // [B, n_q * D]
+  float* partial;             // workspace
+  int B, n_q, n_kv, block, max_ctx;
+};
+size_t dec_attn_partial_floats(int B, int n_q, int D, int max_ctx, int n_kv);
+template <typename T>
+hipError_t decode_attention(const DecAttnArgs& p, int head_dim, hipStream_t s);
+
+// ---- small memory-bound kernels
+// LayerNorm (ln=1, with shift b) or RMSNorm (ln=0) of fp32 rows into T rows.
+// merge>1: row m = (img, py, px) of a (gh, gw) grid goes to merged row (img, py/m, px/m),
+// column block (py%m)*m + px%m; out row stride is then merge*merge*H.
+template <typename T>
+hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln,
+                     T* out, int ldo, int merge, int gh, int gw, hipStream_t s);
+// Image [B, H, W, 3] bf16 -> patch rows [B*gh*gw, kpad] (zero padded), order (py, px, c).
+template <typename T>
+hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* out, hipStream_t s);
+// Split a packed QKV projection.  Rotates q and k in place when rope_theta > 0 (positions
+// pos0 + t), writes V transposed for attention (vt), and when tables != null writes the
+// rotated K and V of every token into the paged cache.
+template <typename T>
+hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0,
+                       T* vt, int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s);
+// Decode: qkv fp32 [B, (n_q+2n_kv)D]; rotate at pos[b]; q -> qout [B, n_q, D]; k, v -> paged cache.
+template <typename T>
+hipError_t qkv_decode(const float* qkv, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos,
+                      T* qout, T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s);
+// x[r] = r < n_vis ? vis[r] : embed[ids[r - n_vis]]  (fp32 out)
+template <typename T>
+hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const bf16_t* embed, int H, float* x,
+                      hipStream_t s);
+hipError_t argmax_rows(const float* logits, int B, int V, int* out, hipStream_t s);
+
+}  // namespace nova
