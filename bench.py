@@ -1,0 +1,360 @@
+"""Benchmark of the single-GPU VLM serving hot path on MI355X.
+
+Headline: vision-encode throughput (patches/s) of the 32-layer, 1280-wide ViT on 1008x1008
+images (5184 patches each, 2x2 merge to 3584) at batch 8 on all 256 CUs.  The same JSON line
+carries per-stage throughput (encode patches/s at batch 1/4/8, prefill tok/s of a 1500-token
+prompt, decode tok/s at batch 1/8/32 on the 28-layer GQA decoder), each stage's throughput
+against its CU share (XCD-balanced masks of 32..256 CUs), decode co-running with encode and
+with prefill on complementary partitions, the roofline position of the dominant kernel family,
+and the oracle's CPU time on a bounded sample.
+
+All inputs are seeded synthetic data of the workload shapes; weights are random N(0, 0.02)
+bf16 generated on the device.  Usage: python bench.py [--steps K] [--warmup W] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ----------------------------------------------------------------------------- model builders
+def random_blob(nbytes, offsets, norm_idx, device, gen, std=0.02):
+    """A packed weight blob of N(0, std) bf16 with the norm-gain tensors set to 1 + N(0, 0.2)."""
+    import torch
+    t = (torch.randn(nbytes // 2, generator=gen, device=device, dtype=torch.float32) * std).to(torch.bfloat16)
+    return t
+
+
+def build_vit(nova, cfg, device, seed=0, n_slots=0):
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    (eo, eb), (lo, lb), (ho, hb) = nova.vit_layouts(cfg)
+    H = cfg.hidden
+    emb = random_blob(eb, eo, [], device, gen)
+    layers = random_blob(lb * cfg.layers, lo, [], device, gen)
+    head = random_blob(hb, ho, [], device, gen)
+    lv = layers.view(cfg.layers, lb // 2)
+    for i in (0, 6):      # ln1.g, ln2.g
+        lv[:, lo[i] // 2: lo[i] // 2 + H] = 1.0
+    head[ho[0] // 2: ho[0] // 2 + H] = 1.0
+    if n_slots > 0:
+        host = torch.empty(layers.numel(), dtype=torch.bfloat16, pin_memory=True)
+        host.copy_(layers)
+        layers = host
+    return nova.Vit(cfg, None, blobs=(emb, layers, head, lb), n_slots=n_slots)
+
+
+def build_llm(nova, cfg, device, seed=1):
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    (lo, lb), (ho, hb) = nova.llm_layouts(cfg)
+    H = cfg.hidden
+    layers = random_blob(lb * cfg.layers, lo, [], device, gen)
+    lv = layers.view(cfg.layers, lb // 2)
+    for i in (0, 3):      # rms1.g, rms2.g
+        lv[:, lo[i] // 2: lo[i] // 2 + H] = 1.0
+    head = random_blob(hb, ho, [], device, gen)
+    head[ho[0] // 2: ho[0] // 2 + H] = 1.0
+    embed = (torch.randn(cfg.vocab * H, generator=gen, device=device) * 0.02).to(torch.bfloat16).view(cfg.vocab, H)
+    return nova.Llm(cfg, None, blobs=(embed, layers, head, lb))
+
+
+# ----------------------------------------------------------------------------- work counts
+def vit_flops(cfg, batch):
+    """Algorithmic FLOPs of one encode pass: GEMMs (patch embed, 4 linears per layer, adapter) and attention."""
+    n, H, I = cfg.n_patches, cfg.hidden, cfg.mlp
+    lin_layer = 2 * n * H * (3 * H + H + I + I)
+    attn_layer = 4 * n * n * H
+    embed = 2 * n * cfg.patch_dim * H
+    merge = 2 * cfg.n_out * (cfg.merge ** 2 * H) * cfg.out_hidden
+    gemm = cfg.layers * lin_layer + embed + merge
+    return batch * gemm, batch * cfg.layers * attn_layer
+
+
+def prefill_flops(cfg, s):
+    H, d = cfg.hidden, cfg.head_dim
+    lin = 2 * s * H * ((cfg.n_q + 2 * cfg.n_kv) * d + cfg.n_q * d + 3 * cfg.inter) * cfg.layers
+    attn = 2 * s * s * cfg.n_q * d * cfg.layers          # causal: half of 4 S^2 n_q d
+    head = 2 * H * cfg.vocab
+    return lin + head, attn
+
+
+def decode_bytes(cfg, batch, ctx):
+    """Algorithmic HBM bytes of one decode step: every weight once plus each sequence's K/V."""
+    H, d, I = cfg.hidden, cfg.head_dim, cfg.inter
+    w_layer = (H * (cfg.n_q + 2 * cfg.n_kv) * d + H * cfg.n_q * d + 3 * H * I + 2 * H) * 2
+    weights = cfg.layers * w_layer + (cfg.vocab * H + H) * 2 + batch * H * 2
+    kv = batch * ctx * cfg.layers * cfg.n_kv * d * 2 * 2
+    return weights, kv
+
+
+# ----------------------------------------------------------------------------- timing helpers
+def time_passes(torch, fn, reps, stream):
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+class Stages:
+    """The three stage workloads on one GPU, each callable on a given stream."""
+
+    def __init__(self, nova, torch, synth, device, enc_batch):
+        self.nova, self.torch = nova, torch
+        self.vc, self.lc = synth.VIT_1008, synth.LLM_28
+        log("building ViT-32 (1008x1008) and LLM-28 random weights on the device")
+        self.vit = build_vit(nova, self.vc, device)
+        self.llm = build_llm(nova, self.lc, device)
+        img = synth.image(enc_batch, self.vc.image_h, self.vc.image_w, seed=1)
+        self.pixels = torch.from_numpy(img).to(device, torch.bfloat16).contiguous()
+        self.enc_out = torch.empty(self.vit.out_shape(enc_batch), dtype=torch.bfloat16, device=device)
+        # prefill: 1300 vision embeddings + 200 text ids
+        nv, nt = synth.LLM_VISION_TOKENS, synth.LLM_TEXT_TOKENS
+        self.s = nv + nt
+        self.vis = torch.from_numpy(synth.vision_embeds(nv, self.lc.hidden)).to(device, torch.bfloat16)
+        self.ids = torch.from_numpy(synth.text_ids(nt, self.lc.vocab)).to(device)
+        # KV pool for 32 sequences of up to 1500 + 64 tokens, plus one prefill sequence
+        self.ctx_max = self.s + synth.LLM_DECODE_STEPS
+        self.bmax = 32
+        tables, pool = synth.block_tables([self.ctx_max] * (self.bmax + 1), self.lc.block, seed=5)
+        self.pool = pool
+        self.kv = nova.KvPool(self.llm, pool)
+        g = torch.Generator(device=device)
+        g.manual_seed(7)
+        self.kv.k.copy_((torch.randn(self.kv.k.numel(), generator=g, device=device) * 0.5).to(self.kv.k.dtype))
+        self.kv.v.copy_((torch.randn(self.kv.v.numel(), generator=g, device=device) * 0.5).to(self.kv.v.dtype))
+        self.tables = torch.from_numpy(tables).to(device)
+        self.pre_table = self.tables[self.bmax]
+        self.dec_ids = torch.from_numpy(synth.text_ids(self.bmax, self.lc.vocab, seed=9)).to(device)
+        self.dec_pos = torch.full((self.bmax,), self.s, dtype=torch.int32, device=device)
+        self.next_ids = torch.empty(self.bmax, dtype=torch.int32, device=device)
+        self.pre_next = torch.empty(1, dtype=torch.int32, device=device)
+        # warm every workspace once
+        torch.cuda.synchronize()
+
+    def encode(self, batch=None, stream=None):
+        px = self.pixels if batch is None else self.pixels[:batch]
+        out = self.enc_out if batch is None else self.enc_out[:batch]
+        self.vit.encode(px, out=out, stream=stream)
+
+    def prefill(self, stream=None):
+        self.llm.prefill(self.vis, self.ids, self.pre_table, self.kv, next_id=self.pre_next, stream=stream)
+
+    def decode(self, batch, stream=None):
+        self.llm.decode(self.dec_ids[:batch], self.dec_pos[:batch], self.tables[:batch], self.kv, self.ctx_max,
+                        next_ids=self.next_ids[:batch], stream=stream)
+
+
+# ----------------------------------------------------------------------------- CPU baseline
+def cpu_baseline(synth):
+    """The oracle, as is, on one image's worth of encoder layers at the real shape (2 of 32
+    layers plus the adapter), extrapolated to a full 32-layer pass."""
+    from oracle import vlm
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    cfg = synth.VIT_1008
+    names = ["patch.w", "patch.b", "pos", "merge.ln.g", "merge.ln.b", "merge.w", "merge.b"]
+    names += synth.vit_layer_names(0)
+    w = synth.vit_weights(cfg, seed=0, names=names)
+    img = synth.image(1, cfg.image_h, cfg.image_w, seed=1)[0]
+    t0 = time.perf_counter()
+    x = vlm.patch_embed(img, w, cfg)
+    t_embed = time.perf_counter() - t0
+    layers_timed = 2
+    t0 = time.perf_counter()
+    for _ in range(layers_timed):
+        x = vlm.vit_layer(x, w, 0, cfg)
+    t_layer = (time.perf_counter() - t0) / layers_timed
+    t0 = time.perf_counter()
+    vlm.merge_adapter(x, w, cfg)
+    t_merge = time.perf_counter() - t0
+    t_img = t_embed + cfg.layers * t_layer + t_merge
+    return {"value": round(cfg.n_patches / t_img, 2), "unit": "patches/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"1 image of {cfg.image_h}x{cfg.image_w} ({cfg.n_patches} patches): patch embed, "
+                      f"{layers_timed} of {cfg.layers} encoder layers timed (float64 NumPy), adapter; "
+                      f"full pass extrapolated as embed + {cfg.layers} x layer + adapter = {t_img:.1f} s"}
+
+
+# ----------------------------------------------------------------------------- main
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--batch", type=int, default=8, help="images per encode pass (headline)")
+    ap.add_argument("--no-sweep", action="store_true", help="skip CU-share curves and co-run")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the method serves all three stages on a single GPU; "
+              "multi-GPU runs are not part of this build (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2509_21301_amd import nova, synth
+    device = "cuda"
+    nova.init(0)
+    st = Stages(nova, torch, synth, device, args.batch)
+    vc, lc = st.vc, st.lc
+    B = args.batch
+    stream = torch.cuda.current_stream()
+
+    # ---------------- headline: encode, batch B, all CUs
+    for _ in range(args.warmup):
+        st.encode()
+    torch.cuda.synchronize()
+    nova.timing_enable(True)
+    for k in nova.KIND_NAMES:
+        nova.timing_read(k)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        st.encode()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1)
+    kinds = {nova.KIND_NAMES[k]: nova.timing_read(k) for k in nova.KIND_NAMES}
+    nova.timing_enable(False)
+    ms_step = ms / args.steps
+    value = B * vc.n_patches * args.steps / (ms / 1e3)
+    gemm_f, attn_f = vit_flops(vc, B)
+    log(f"encode batch {B}: {ms_step:.2f} ms/pass, {value:.0f} patches/s, "
+        f"{(gemm_f + attn_f) / (ms_step / 1e3) / 1e12:.1f} TFLOP/s overall (wall {wall:.2f}s)")
+    for nm, (t, n) in kinds.items():
+        log(f"  {nm:18s} {t / args.steps:9.3f} ms/pass  {n / args.steps:6.1f} launches/pass")
+    # dominant kernel family of the pass and its roofline position
+    fam_flops = {"gemm": gemm_f, "attention": attn_f}
+    dom = max(fam_flops, key=lambda f: kinds[f][0])
+    t_dom, n_dom = kinds[dom]
+    flops_per_launch = fam_flops[dom] * args.steps / max(n_dom, 1)
+    achieved = flops_per_launch / ((t_dom / max(n_dom, 1)) / 1e3) / 1e12
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "avg_launch_ms": round(t_dom / max(n_dom, 1), 4),
+                "flops_per_launch": flops_per_launch,
+                "other_kernels": {f: round(fam_flops[f] * args.steps / kinds[f][0] / 1e9, 1)
+                                  for f in fam_flops if f != dom and kinds[f][0] > 0}}
+
+    result = {
+        "metric": "per-stage tok/s and patches/s vs CU share; co-run max latency at 1 GPU",
+        "value": round(value, 1), "unit": "patches/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded uniform-noise images, random N(0,0.02) bf16 weights)",
+        "config": {"workload": f"vision encode, ViT 32x1280 (16 heads, MLP 5120, patch 14, 2x2 merge to 3584), "
+                               f"{B} images of {vc.image_h}x{vc.image_w} ({vc.n_patches} patches each) per step",
+                   "global_batch": B, "seq_len": vc.n_patches, "parallelism": "single GPU, 256 CUs"},
+        "roofline": roofline,
+    }
+    if args.only_encode:
+        print(json.dumps(result), flush=True)
+        return
+
+    # ---------------- per-stage throughput on all CUs
+    stages = {}
+    for b in (1, 4, 8):
+        if b > B:
+            continue
+        t = time_passes(torch, lambda: st.encode(b), 3, stream)
+        stages[f"encode_b{b}"] = {"ms": round(t, 3), "patches_per_s": round(b * vc.n_patches / (t / 1e3), 1),
+                                  "tflops": round(sum(vit_flops(vc, b)) / (t / 1e3) / 1e12, 1)}
+    st.prefill()
+    t = time_passes(torch, st.prefill, 5, stream)
+    pf_lin, pf_attn = prefill_flops(lc, st.s)
+    stages["prefill_s1500"] = {"ms": round(t, 3), "tok_per_s": round(st.s / (t / 1e3), 1),
+                               "tflops": round((pf_lin + pf_attn) / (t / 1e3) / 1e12, 1)}
+    for b in (1, 8, 32):
+        st.decode(b)
+        t = time_passes(torch, lambda: st.decode(b), 10, stream)
+        wb, kvb = decode_bytes(lc, b, st.ctx_max)
+        stages[f"decode_b{b}"] = {"ms": round(t, 3), "tok_per_s": round(b / (t / 1e3), 1),
+                                  "hbm_gbs": round((wb + kvb) / (t / 1e3) / 1e9, 1),
+                                  "hbm_frac": round((wb + kvb) / (t / 1e3) / 1e9 / HBM_PEAK_GBS, 3)}
+    result["stages"] = stages
+    log(json.dumps(stages))
+
+    # ---------------- CU-share curves and co-run (XCD-balanced partitions)
+    if not args.no_sweep:
+        shares = [32, 64, 96, 128, 160, 192, 224, 256]
+        curves = {"shares": shares, "encode_b1_patches_per_s": [], "prefill_tok_per_s": [], "decode_b8_tok_per_s": []}
+        for p in shares:
+            ms_e = ms_p = ms_d = None
+            s_e = nova.set_stage_partition(nova.STAGE_ENCODE, nova.make_cu_mask(p, 0))
+            ms_e = time_passes(torch, lambda: st.encode(1, stream=s_e), 2, s_e)
+            s_p = nova.set_stage_partition(nova.STAGE_PREFILL, nova.make_cu_mask(p, 0))
+            ms_p = time_passes(torch, lambda: st.prefill(stream=s_p), 2, s_p)
+            s_d = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(p, 0))
+            ms_d = time_passes(torch, lambda: st.decode(8, stream=s_d), 5, s_d)
+            curves["encode_b1_patches_per_s"].append(round(vc.n_patches / (ms_e / 1e3), 1))
+            curves["prefill_tok_per_s"].append(round(st.s / (ms_p / 1e3), 1))
+            curves["decode_b8_tok_per_s"].append(round(8 / (ms_d / 1e3), 1))
+            log(f"share {p:3d} CUs: encode {ms_e:.2f} ms, prefill {ms_p:.2f} ms, decode(b8) {ms_d:.3f} ms")
+        result["cu_share_curves"] = curves
+        # co-run: decode (batch 8) on P CUs with encode (batch 1) or prefill on the other 256 - P
+        corun = []
+        for other in ("encode", "prefill"):
+            for p in [32, 64, 96, 128, 160, 192, 224]:
+                s_d = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(p, 0))
+                so = nova.set_stage_partition(nova.STAGE_ENCODE if other == "encode" else nova.STAGE_PREFILL,
+                                              nova.make_cu_mask(256 - p, p // 8))
+                run_other = (lambda: st.encode(1, stream=so)) if other == "encode" else (lambda: st.prefill(stream=so))
+                torch.cuda.synchronize()
+                t_o = time_passes(torch, run_other, 1, so)          # solo on its partition (warm)
+                n_dec = 40
+                torch.cuda.synchronize()
+                eo0, eo1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ed0, ed1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                eo0.record(so)
+                run_other()
+                eo1.record(so)
+                ed0.record(s_d)
+                for _ in range(n_dec):
+                    st.decode(8, stream=s_d)
+                ed1.record(s_d)
+                torch.cuda.synchronize()
+                t_oc = eo0.elapsed_time(eo1)
+                t_dc = ed0.elapsed_time(ed1) / n_dec
+                corun.append({"pair": f"decode+{other}", "decode_cus": p, "other_cus": 256 - p,
+                              f"{other}_ms_solo_on_partition": round(t_o, 3), f"{other}_ms_corun": round(t_oc, 3),
+                              "decode_step_ms_corun": round(t_dc, 3)})
+                log(f"co-run decode {p} / {other} {256 - p}: {other} {t_oc:.2f} ms (solo {t_o:.2f}), decode step {t_dc:.3f} ms")
+        result["corun"] = corun
+
+    if not args.no_cpu:
+        log("timing the oracle on the host (bounded sample)")
+        result["cpu_baseline"] = cpu_baseline(synth)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
