@@ -211,6 +211,8 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip CU-share curves and co-run")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
+    ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32"],
+                    help="run only this stage in a loop of --steps passes (for rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the method serves all three stages on a single GPU; "
@@ -225,6 +227,14 @@ def main():
     vc, lc = st.vc, st.lc
     B = args.batch
     stream = torch.cuda.current_stream()
+
+    if args.profile_stage:
+        fn = st.prefill if args.profile_stage == "prefill" else (lambda: st.decode(int(args.profile_stage[6:])))
+        for _ in range(args.warmup):
+            fn()
+        ms = time_passes(torch, fn, args.steps, stream)
+        log(f"{args.profile_stage}: {ms:.3f} ms per pass")
+        return
 
     # ---------------- headline: encode, batch B, all CUs
     for _ in range(args.warmup):

@@ -23,7 +23,7 @@ constexpr int AQ = 128;   // queries per workgroup
 constexpr int AK = 64;    // keys per tile
 
 template <typename T, int D, bool CAUSAL>
-__global__ void __launch_bounds__(256) attn_kernel(AttnArgs p) {
+__global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   constexpr bool F32 = sizeof(T) == 4;
   constexpr int NS = D / 16;                // k-steps of QK^T
   constexpr int DP = (D + 31) / 32 * 32;    // output rows padded to 32
@@ -166,37 +166,47 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnArgs p) {
         }
       }
     }
-    // online softmax for query qrow: keys kv0 + 32kb + 8(r/4) + 4g + r%4
+    // online softmax for query qrow over keys kv0 + 32kb + 8(r/4) + 4g + r%4; the running max is
+    // kept in raw score units and the 1/sqrt(d) scale is folded into the exp2 argument.
+    const bool need_mask = (kv0 + AK > p.sk) || (CAUSAL && kv0 + AK - 1 > q0 + wave * 32);
+    if (need_mask) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kidx = kv0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+          const bool ok = kidx < p.sk && (!CAUSAL || kidx <= qrow);
+          sacc[kb][r] = ok ? sacc[kb][r] : -INFINITY;
+        }
+    }
     float tmax = -1e30f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kidx = kv0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-        const bool ok = kidx < p.sk && (!CAUSAL || kidx <= qrow);
-        const float sv = ok ? sacc[kb][r] * scale : -INFINITY;
-        sacc[kb][r] = sv;
-        tmax = fmaxf(tmax, sv);
-      }
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[kb][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float m_new = fmaxf(m_run, tmax);
-    const float corr = exp2f(m_run - m_new);
+    const float ms = m_new * scale;
     float rsum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float pv = exp2f(sacc[kb][r] - m_new);
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[kb][r], scale, -ms));
         sacc[kb][r] = pv;
         rsum += pv;
       }
     rsum += __shfl_xor(rsum, 32, 64);
-    l_run = l_run * corr + rsum;
+    if (__ballot(m_new > m_run)) {       // rescale only when some query's max moved
+      const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * scale);
+      l_run *= corr;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[c][r] *= corr;
+    }
+    l_run += rsum;
     m_run = m_new;
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[c][r] *= corr;
 
     // O^T += V^T P^T, 16 keys per MFMA
 #pragma unroll
@@ -268,7 +278,9 @@ hipError_t attention(const AttnArgs& p, int head_dim, hipStream_t s) {
   switch (head_dim) {
     case 64: return attn_launch<T, 64>(p, s);
     case 80: return attn_launch<T, 80>(p, s);
-    case 128: return attn_launch<T, 128>(p, s);
+    case 128:
+      if constexpr (sizeof(T) == 2) return attn_launch<T, 128>(p, s);   // fp32 mode stops at d = 80
+      break;
   }
   return hipErrorInvalidValue;
 }

@@ -20,11 +20,11 @@ constexpr int PAD = 8;             // bf16 elements of row padding in LDS
 constexpr int LDK = BK + PAD;      // LDS row pitch (elements)
 
 template <typename TA, typename OT, int EPI, int BM, int BN, int WM, int WN>
-__global__ void __launch_bounds__(256) gemm_kernel(GemmArgs p) {
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_kernel(GemmArgs p) {
   constexpr bool F32A = sizeof(TA) == 4;
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int WAVES_N = BN / WN;
-  static_assert((BM / WM) * (BN / WN) == 4, "four waves");
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;     // threads per workgroup
   extern __shared__ __align__(16) unsigned char smem[];
   bf16_t* As = reinterpret_cast<bf16_t*>(smem);                 // [2][BM][LDK] (x2 for hi/lo)
   constexpr int A_ELEMS = BM * LDK * (F32A ? 2 : 1);
@@ -51,22 +51,23 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs p) {
   // ---- global -> register staging
   constexpr int A_CHUNK = F32A ? 4 : 8;                 // elements per 16-byte chunk
   constexpr int A_CPR = BK / A_CHUNK;                   // chunks per row
-  constexpr int A_ITERS = BM * A_CPR / 256;
-  constexpr int B_ITERS = BN * (BK / 8) / 256;
+  constexpr int A_ITERS = BM * A_CPR / NT;
+  constexpr int B_ITERS = BN * (BK / 8) / NT;
+  static_assert(A_ITERS * NT == BM * A_CPR && B_ITERS * NT == BN * (BK / 8), "tile/thread mismatch");
   u32x4 ra[A_ITERS], rb[B_ITERS];
   const TA* Ag = reinterpret_cast<const TA*>(p.A);
 
   auto load_global = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < A_ITERS; ++i) {
-      int c = tid + i * 256, row = c / A_CPR, col = (c % A_CPR) * A_CHUNK;
+      int c = tid + i * NT, row = c / A_CPR, col = (c % A_CPR) * A_CHUNK;
       int m = m0 + row;
       if (m < p.M) ra[i] = *reinterpret_cast<const u32x4*>(Ag + (size_t)m * p.lda + k0 + col);
       else ra[i] = u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int i = 0; i < B_ITERS; ++i) {
-      int c = tid + i * 256, row = c / (BK / 8), col = (c % (BK / 8)) * 8;
+      int c = tid + i * NT, row = c / (BK / 8), col = (c % (BK / 8)) * 8;
       rb[i] = *reinterpret_cast<const u32x4*>(p.W + (size_t)(n0 + row) * p.ldw + k0 + col);
     }
   };
@@ -75,7 +76,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs p) {
     bf16_t* b = Bs + buf * B_ELEMS;
 #pragma unroll
     for (int i = 0; i < A_ITERS; ++i) {
-      int c = tid + i * 256, row = c / A_CPR, col = (c % A_CPR) * A_CHUNK;
+      int c = tid + i * NT, row = c / A_CPR, col = (c % A_CPR) * A_CHUNK;
       if constexpr (F32A) {
         float x[4] = {__uint_as_float(ra[i][0]), __uint_as_float(ra[i][1]), __uint_as_float(ra[i][2]),
                       __uint_as_float(ra[i][3])};
@@ -93,7 +94,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs p) {
     }
 #pragma unroll
     for (int i = 0; i < B_ITERS; ++i) {
-      int c = tid + i * 256, row = c / (BK / 8), col = (c % (BK / 8)) * 8;
+      int c = tid + i * NT, row = c / (BK / 8), col = (c % (BK / 8)) * 8;
       *reinterpret_cast<u32x4*>(b + row * LDK + col) = rb[i];
     }
   };
@@ -195,16 +196,17 @@ static hipError_t launch_tile(const GemmArgs& p, hipStream_t s) {
     attr_set = true;
   }
   const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
-  hipLaunchKernelGGL(kern, dim3(nm * nn), dim3(256), lds, s, p);
+  hipLaunchKernelGGL(kern, dim3(nm * nn), dim3((BM / WM) * (BN / WN) * 64), lds, s, p);
   return hipGetLastError();
 }
 
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
-  // Larger tiles when there are enough of them to fill 256 CUs.
+  // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when N is wide and there are at least
+  // two tiles per CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU).
   if constexpr (sizeof(TA) == 2) {
-    const long tiles_big = (long)((p.M + 255) / 256) * (p.N / 128);
-    if (tiles_big >= 256) return launch_tile<TA, OT, EPI, 256, 128, 128, 64>(p, s);
+    const long tiles = (long)((p.M + 255) / 256) * (p.N / 256);
+    if (p.N % 256 == 0 && p.N >= 3072 && tiles >= 512) return launch_tile<TA, OT, EPI, 256, 256, 64, 128>(p, s);
   }
   return launch_tile<TA, OT, EPI, 128, 128, 64, 64>(p, s);
 }

@@ -1,21 +1,21 @@
 // Thin GEMM for the decode linears and the LM head: Y[B,N] = X[B,K] W[N,K]^T, B <= 32.
 //
 // Decode is bound by streaming the weights from HBM (the paper's Table 3 decode row and
-// Sec. 3.2.1).  Each wave streams 32 weight rows with 16-byte loads, 128 contiguous bytes per
-// lane per 256-wide K chunk (16 loads in flight per lane), and feeds them to MFMA 16x16x32 as
+// Sec. 3.2.1).  Each wave streams 32 weight rows with 16-byte loads (16 per lane per 256-wide
+// K chunk, 32 in flight with the prefetch), and feeds them to MFMA 16x16x32 as
 // the A operand with the batch as the 16-wide B operand (a second MFMA covers rows 16..31 of
-// the batch).  X chunks are staged in LDS once per workgroup.  When N alone gives too few
-// workgroups, K is split and a small second pass reduces the fp32 partials and applies the
+// the batch).  X fragments come straight from L2 (X is small and shared by every workgroup);
+// weight loads run one chunk ahead of the MFMAs, with no LDS and no barriers.  When N alone
+// gives too few workgroups, K is split and a small second pass reduces the fp32 partials and applies the
 // epilogue; otherwise the epilogue is applied directly.
-// The k index of an MFMA fragment only has to agree between its A and B operands, so each
-// lane can read 128 contiguous bytes of its row and use them as eight consecutive fragments.
+// The k index of an MFMA fragment only has to agree between its A and B operands, which leaves
+// the assignment of k pieces to lanes free; it is chosen for coalescing.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace nova {
 
-constexpr int GV_KC = 256;          // K chunk staged per iteration
-constexpr int GV_XP = GV_KC + 8;    // LDS row pitch of the X chunk (bf16 elements)
+constexpr int GV_KC = 256;          // K chunk per pipeline step
 constexpr int GV_ROWS = 128;        // weight rows per workgroup (4 waves x 32)
 
 int gemv_splits(int N, int K) {
@@ -35,13 +35,14 @@ size_t gemv_partial_floats(int B, int N, int K) {
 template <typename TX, typename OT, int NB, int EPI, bool DIRECT>
 __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
   constexpr bool F32X = sizeof(TX) == 4;
-  __shared__ __align__(16) bf16_t xs[(F32X ? 2 : 1) * 32 * GV_XP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_base = blockIdx.x * GV_ROWS + wave * 32;
   const int split = blockIdx.y;
-  const int k_begin = split * kc;
+  const int k_begin = split * kc, k_end = k_begin + kc;
   const int row = lane & 15, g = lane >> 4;
-  const bf16_t* w0 = p.W + (size_t)(n_base + row) * p.ldw;
+  // Fragment u of a 256-wide chunk holds k = k0 + 8 * (4u + g) .. +8: the four lanes of a row
+  // read 64 adjacent bytes per instruction and two instructions complete each 128-byte line.
+  const bf16_t* w0 = p.W + (size_t)(n_base + row) * p.ldw + 8 * g;
   const bf16_t* w1 = w0 + (size_t)16 * p.ldw;
   const TX* X = reinterpret_cast<const TX*>(p.X);
 
@@ -51,57 +52,54 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = k_begin; k0 < k_begin + kc; k0 += GV_KC) {
-    // weight fragments for this chunk: 128 contiguous bytes of each of the lane's two rows
-    u32x4 wa[8], wb[8];
-    const u32x4* pa = reinterpret_cast<const u32x4*>(w0 + k0 + g * 64);
-    const u32x4* pb = reinterpret_cast<const u32x4*>(w1 + k0 + g * 64);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) { wa[u] = __builtin_nontemporal_load(pa + u); wb[u] = __builtin_nontemporal_load(pb + u); }
-    // stage X[0..31][k0..k0+255] (rows >= B are zero)
-    __syncthreads();
-    if constexpr (F32X) {
-      for (int c = tid; c < 32 * GV_KC / 4; c += 256) {
-        const int b = c / (GV_KC / 4), col = (c % (GV_KC / 4)) * 4;
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        if (b < p.B) {
-          float4 t = *reinterpret_cast<const float4*>(X + (size_t)b * p.ldx + k0 + col);
-          v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-        }
-        bf16_t h[4];
-        float l[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) { h[j] = f2bf(v[j]); l[j] = v[j] - bf2f(h[j]); }
-        *reinterpret_cast<uint2*>(xs + b * GV_XP + col) =
-            make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
-        *reinterpret_cast<uint2*>(xs + 32 * GV_XP + b * GV_XP + col) = make_uint2(pack2(l[0], l[1]), pack2(l[2], l[3]));
-      }
-    } else {
-      for (int c = tid; c < 32 * GV_KC / 8; c += 256) {
-        const int b = c / (GV_KC / 8), col = (c % (GV_KC / 8)) * 8;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (b < p.B) v = *reinterpret_cast<const uint4*>(X + (size_t)b * p.ldx + k0 + col);
-        *reinterpret_cast<uint4*>(xs + b * GV_XP + col) = v;
-      }
-    }
-    __syncthreads();
+  auto load_w = [&](int k0, u32x4 (&wa)[8], u32x4 (&wb)[8]) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int kk = g * 64 + u * 8;
-      Frag8 fa = __builtin_bit_cast(Frag8, wa[u]);
-      Frag8 fb = __builtin_bit_cast(Frag8, wb[u]);
+      wa[u] = *reinterpret_cast<const u32x4*>(w0 + k0 + 32 * u);
+      wb[u] = *reinterpret_cast<const u32x4*>(w1 + k0 + 32 * u);
+    }
+  };
+  auto compute = [&](int k0, const u32x4 (&wa)[8], const u32x4 (&wb)[8]) {
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        Frag8 fx = *reinterpret_cast<const Frag8*>(xs + (j * 16 + row) * GV_XP + kk);
-        acc[0][j] = mfma16(fa, fx, acc[0][j]);
-        acc[1][j] = mfma16(fb, fx, acc[1][j]);
+    for (int j = 0; j < NB; ++j) {
+      const int b = j * 16 + row;
+      const TX* xr = X + (size_t)b * p.ldx + k0 + 8 * g;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        Frag8 fx, fl;
+        if (b < p.B) {
+          if constexpr (F32X) {
+            float x8[8];
+            *reinterpret_cast<float4*>(x8) = *reinterpret_cast<const float4*>(xr + 32 * u);
+            *reinterpret_cast<float4*>(x8 + 4) = *reinterpret_cast<const float4*>(xr + 32 * u + 4);
+            split8(x8, fx, fl);
+          } else {
+            fx = *reinterpret_cast<const Frag8*>(xr + 32 * u);
+          }
+        } else {
+          fx = zero_frag();
+          if constexpr (F32X) fl = zero_frag();
+        }
+        acc[0][j] = mfma16(__builtin_bit_cast(Frag8, wa[u]), fx, acc[0][j]);
+        acc[1][j] = mfma16(__builtin_bit_cast(Frag8, wb[u]), fx, acc[1][j]);
         if constexpr (F32X) {
-          Frag8 fl = *reinterpret_cast<const Frag8*>(xs + 32 * GV_XP + (j * 16 + row) * GV_XP + kk);
-          acc[0][j] = mfma16(fa, fl, acc[0][j]);
-          acc[1][j] = mfma16(fb, fl, acc[1][j]);
+          acc[0][j] = mfma16(__builtin_bit_cast(Frag8, wa[u]), fl, acc[0][j]);
+          acc[1][j] = mfma16(__builtin_bit_cast(Frag8, wb[u]), fl, acc[1][j]);
         }
       }
     }
+  };
+
+  // two chunks per trip: the loads of the next chunk are in flight while this one computes
+  u32x4 wa0[8], wb0[8], wa1[8], wb1[8];
+  load_w(k_begin, wa0, wb0);
+  for (int k0 = k_begin; k0 < k_end; k0 += 2 * GV_KC) {
+    const bool has1 = k0 + GV_KC < k_end;
+    if (has1) load_w(k0 + GV_KC, wa1, wb1);
+    compute(k0, wa0, wb0);
+    if (!has1) break;
+    if (k0 + 2 * GV_KC < k_end) load_w(k0 + 2 * GV_KC, wa0, wb0);
+    compute(k0 + GV_KC, wa1, wb1);
   }
 
   // lane holds D[n = 4*(lane/16) + r][b = lane%16] of each 16x16 tile
