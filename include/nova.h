@@ -135,8 +135,8 @@ typedef struct {
 
 /* layer blob: 0 rms1.g [hidden], 1 qkv.w [(n_q+2n_kv)*head_dim, hidden] (q | k | v, head-major),
  *             2 o.w [hidden, n_q*head_dim], 3 rms2.g [hidden],
- *             4 gu.w [2*ip, hidden]: gate and up rows interleaved in blocks of 16
- *               (rows 32j..32j+15 = gate rows 16j..16j+15, rows 32j+16..32j+31 = up rows 16j..),
+ *             4 gu.w [2*ip, hidden]: gate and up rows interleaved in blocks of 8
+ *               (rows 16j..16j+7 = gate rows 8j..8j+7, rows 16j+8..16j+15 = up rows 8j..8j+7),
  *             5 down.w [hidden, ip]      (ip = inter rounded up to 256; padding is zero)
  * head blob:  0 norm.g [hidden], 1 lm_head.w [vocab, hidden]
  * The embedding table is a separate device bf16 [vocab, hidden] array. */

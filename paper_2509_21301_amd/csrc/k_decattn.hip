@@ -23,7 +23,9 @@ static int dec_splits(int B, int n_kv, int max_ctx) {
   const int want = (512 + B * n_kv - 1) / (B * n_kv);
   int per = (pairs + want - 1) / want;                  // block pairs per split
   per = max(per, DA_TOK_PER_SPLIT_MIN / 32);
-  return (pairs + per - 1) / per;
+  int n = (pairs + per - 1) / per;
+  while (n > 64) n = (pairs + ++per - 1) / per;      // the combine holds at most 64 splits
+  return n;
 }
 
 size_t dec_attn_partial_floats(int B, int n_q, int D, int max_ctx, int n_kv) {
@@ -203,19 +205,28 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
   }
 }
 
+// Log-sum-exp combine of the context splits: one workgroup of D threads per (sequence, head);
+// split statistics are read in parallel, then every thread sums its dimension over the splits.
 template <typename T, int D>
-__global__ void dec_attn_combine(DecAttnArgs p, int nsplit) {
+__global__ void __launch_bounds__(D) dec_attn_combine(DecAttnArgs p, int nsplit) {
+  __shared__ float wts[64];
+  __shared__ float norm;
   const int bh = blockIdx.x;                 // b * n_q + head
   const float* part = p.partial + (size_t)bh * nsplit * (D + 2);
-  float M = -1e30f;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, part[s * (D + 2)]);
-  float L = 0.f;
-  for (int s = 0; s < nsplit; ++s) L += exp2f(part[s * (D + 2)] - M) * part[s * (D + 2) + 1];
-  for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    float O = 0.f;
-    for (int s = 0; s < nsplit; ++s) O += exp2f(part[s * (D + 2)] - M) * part[s * (D + 2) + 2 + d];
-    reinterpret_cast<T*>(p.out)[(size_t)bh * D + d] = from_f<T>(O / L);
+  const int t = threadIdx.x;
+  float m = -1e30f;
+  if (t < nsplit) m = part[t * (D + 2)];
+  float M = wave_max(t < 64 ? m : -1e30f);
+  if (t < 64) {
+    const float w = t < nsplit ? exp2f(m - M) : 0.f;
+    const float lw = wave_sum(t < nsplit ? w * part[t * (D + 2) + 1] : 0.f);
+    wts[t] = w;
+    if (t == 0) norm = 1.0f / lw;
   }
+  __syncthreads();
+  float O = 0.f;
+  for (int sp = 0; sp < nsplit; ++sp) O += wts[sp] * part[sp * (D + 2) + 2 + t];
+  reinterpret_cast<T*>(p.out)[(size_t)bh * D + t] = from_f<T>(O * norm);
 }
 
 template <typename T, int D>
@@ -226,7 +237,7 @@ static hipError_t dec_launch(const DecAttnArgs& p, hipStream_t s) {
   hipLaunchKernelGGL((dec_attn_kernel<T, D>), dim3(nsplit, p.n_kv, p.B), dim3(256), 0, s, p, per);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nsplit == 1) return e;
-  hipLaunchKernelGGL((dec_attn_combine<T, D>), dim3(p.B * p.n_q), dim3(64), 0, s, p, nsplit);
+  hipLaunchKernelGGL((dec_attn_combine<T, D>), dim3(p.B * p.n_q), dim3(D), 0, s, p, nsplit);
   return hipGetLastError();
 }
 

@@ -152,13 +152,15 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_kernel(GemmAr
       const int m = m0 + wm * WM + i * 16 + er + r;
       if (m >= p.M) continue;
       if constexpr (EPI == EPI_SWIGLU) {
-        // W rows interleaved in 16-row blocks: even blocks gate, odd blocks up.
+        // W rows interleaved in blocks of 8: columns 0-7 of each 16-wide tile are gate outputs,
+        // 8-15 the matching up outputs, held by lanes 8 apart
 #pragma unroll
-        for (int j = 0; j < TN; j += 2) {
-          const int n = n0 + wn * WN + j * 16;          // gate block start (multiple of 32)
-          const int oc = (n >> 5) * 16 + ec;
-          float g = acc[i][j][r], u = acc[i][j + 1][r];
-          reinterpret_cast<OT*>(p.out)[(size_t)m * p.ldo + oc] = from_f<OT>(silu(g) * u);
+        for (int j = 0; j < TN; ++j) {
+          const float g = acc[i][j][r], u = __shfl_xor(acc[i][j][r], 8, 64);
+          if (ec < 8) {
+            const int oc = ((n0 + wn * WN + j * 16) >> 1) + ec;
+            reinterpret_cast<OT*>(p.out)[(size_t)m * p.ldo + oc] = from_f<OT>(silu(g) * u);
+          }
         }
       } else {
 #pragma unroll

@@ -179,7 +179,7 @@ hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float
 
 // ------------------------------------------------------------------ decode QKV: rotate, store q, append k/v
 template <typename T>
-__global__ void qkv_decode_kernel(const float* __restrict__ qkv, int B, int n_q, int n_kv, int D, float theta,
+__global__ void qkv_decode_kernel(const float* __restrict__ qkv, int splits, int B, int n_q, int n_kv, int D, float theta,
                                   const int* __restrict__ pos, T* __restrict__ qout, T* __restrict__ kpool,
                                   T* __restrict__ vpool, const int* __restrict__ tables, int max_blocks, int block) {
   const int half = D / 2;
@@ -190,8 +190,13 @@ __global__ void qkv_decode_kernel(const float* __restrict__ qkv, int B, int n_q,
     const int hh = (int)((idx / half) % heads);
     const int b = (int)(idx / ((long)half * heads));
     const int ps = pos[b];
-    const float* e = qkv + (size_t)b * heads * D + (size_t)hh * D;
-    float x1 = e[c], x2 = e[c + half];
+    float x1 = 0.f, x2 = 0.f;
+#pragma unroll 4
+    for (int sp = 0; sp < splits; ++sp) {
+      const float* e = qkv + ((size_t)sp * B + b) * heads * D + (size_t)hh * D;
+      x1 += e[c];
+      x2 += e[c + half];
+    }
     if (hh < n_q + n_kv) {
       float sn, cs;
       rope_sincos(ps, c, D, theta, &sn, &cs);
@@ -220,13 +225,65 @@ __global__ void qkv_decode_kernel(const float* __restrict__ qkv, int B, int n_q,
 }
 
 template <typename T>
-hipError_t qkv_decode(const float* qkv, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos, T* qout,
-                      T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s) {
+hipError_t qkv_decode(const float* qkv, int splits, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos,
+                      T* qout, T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   const long total = (long)B * (n_q + 2 * n_kv) * (D / 2);
   const int grid = (int)std::min<long>((total + 255) / 256, 65536);
-  hipLaunchKernelGGL((qkv_decode_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, B, n_q, n_kv, D, rope_theta, pos, qout,
+  hipLaunchKernelGGL((qkv_decode_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, splits, B, n_q, n_kv, D, rope_theta, pos, qout,
                      kpool, vpool, tables, max_blocks, block);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ decode residual + RMSNorm
+// One 1024-thread workgroup per row: fold the split-K partials of the previous projection into
+// the fp32 residual stream, then normalise the row for the next projection.
+template <typename T>
+__global__ void __launch_bounds__(1024) resid_rmsnorm_kernel(const float* __restrict__ partial, int splits,
+                                                             float* __restrict__ x, int H, const bf16_t* __restrict__ g,
+                                                             float eps, T* __restrict__ a, int lda,
+                                                             unsigned long long* __restrict__ keys) {
+  __shared__ float red[16];
+  const int b = blockIdx.x, B = gridDim.x;
+  if (keys != nullptr && threadIdx.x == 0) keys[b] = 0ull;
+  float* xr = x + (size_t)b * H;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) {
+    float v = xr[c];
+    if (splits > 0) {
+      float acc = 0.f;
+#pragma unroll 8
+      for (int sp = 0; sp < splits; ++sp) acc += partial[((size_t)sp * B + b) * H + c];
+      v += acc;
+      xr[c] = v;
+    }
+    ss += v * v;
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) tot += red[w];
+  const float rstd = rsqrtf(tot / H + eps);
+  for (int c = threadIdx.x; c < H; c += blockDim.x) a[(size_t)b * lda + c] = from_f<T>(xr[c] * rstd * bf2f(g[c]));
+}
+
+template <typename T>
+hipError_t resid_rmsnorm(const float* partial, int splits, float* x, int B, int H, const bf16_t* g, float eps, T* a,
+                         int lda, unsigned long long* keys, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL((resid_rmsnorm_kernel<T>), dim3(B), dim3(1024), 0, s, partial, splits, x, H, g, eps, a, lda, keys);
+  return hipGetLastError();
+}
+
+__global__ void argmax_finish_kernel(const unsigned long long* __restrict__ keys, int B, int* __restrict__ ids) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) ids[b] = (int)~(uint32_t)(keys[b] & 0xffffffffull);
+}
+
+hipError_t argmax_finish(const unsigned long long* keys, int B, int* ids, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_finish_kernel, dim3((B + 63) / 64), dim3(64), 0, s, keys, B, ids);
   return hipGetLastError();
 }
 
@@ -290,8 +347,10 @@ template hipError_t patchify<bf16_t>(const bf16_t*, int, int, int, int, int, bf1
 template hipError_t patchify<float>(const bf16_t*, int, int, int, int, int, float*, hipStream_t);
 template hipError_t qkv_prefill<bf16_t>(bf16_t*, int, int, int, int, int, float, int, bf16_t*, int, bf16_t*, bf16_t*, const int*, int, hipStream_t);
 template hipError_t qkv_prefill<float>(float*, int, int, int, int, int, float, int, float*, int, float*, float*, const int*, int, hipStream_t);
-template hipError_t qkv_decode<bf16_t>(const float*, int, int, int, int, float, const int*, bf16_t*, bf16_t*, bf16_t*, const int*, int, int, hipStream_t);
-template hipError_t qkv_decode<float>(const float*, int, int, int, int, float, const int*, float*, float*, float*, const int*, int, int, hipStream_t);
+template hipError_t qkv_decode<bf16_t>(const float*, int, int, int, int, int, float, const int*, bf16_t*, bf16_t*, bf16_t*, const int*, int, int, hipStream_t);
+template hipError_t qkv_decode<float>(const float*, int, int, int, int, int, float, const int*, float*, float*, float*, const int*, int, int, hipStream_t);
+template hipError_t resid_rmsnorm<bf16_t>(const float*, int, float*, int, int, const bf16_t*, float, bf16_t*, int, unsigned long long*, hipStream_t);
+template hipError_t resid_rmsnorm<float>(const float*, int, float*, int, int, const bf16_t*, float, float*, int, unsigned long long*, hipStream_t);
 template hipError_t embed_rows<bf16_t>(const bf16_t*, int, const int*, int, const bf16_t*, int, float*, hipStream_t);
 template hipError_t embed_rows<float>(const float*, int, const int*, int, const bf16_t*, int, float*, hipStream_t);
 

@@ -11,7 +11,7 @@ typedef uint16_t bf16_t;
 
 namespace nova {
 
-enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_POS = 3, EPI_SWIGLU = 4 };
+enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_POS = 3, EPI_SWIGLU = 4, EPI_ARGMAX = 5 };
 
 // C[M,N] = A[M,K] W[N,K]^T (+bias) with epilogue.  A has element type TA, row stride lda.
 // STORE/GELU/SWIGLU write OT into out (row stride ldo); RESID adds into the fp32 out;
@@ -28,14 +28,18 @@ template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s);
 
 // Thin GEMM for decode (M = B <= 32 rows): weights streamed once, split over K if needed.
-// out gets epilogue epi (STORE: OT [B, ldo]; RESID: fp32 += ; SWIGLU: OT [B, N/2]).
-// partial is fp32 workspace of gemv_partial_floats() floats.
+// out gets epilogue epi (STORE: OT [B, ldo]; RESID: fp32 += ; SWIGLU: OT [B, N/2];
+// ARGMAX: optional fp32 logits in out, greedy argmax merged into argmax_keys[b], which must be
+// zero beforehand; argmax_finish() turns the keys into token ids).
+// partial is fp32 workspace of gemv_partial_floats() floats laid out [split][B][N].  With
+// gemv_splits() > 1 and out == null the partials are left for the caller's fused reduction.
 struct GemvArgs {
   const void* X; int ldx;
   const bf16_t* W; int ldw;
   int B, N, K;
   void* out; int ldo;
   float* partial;
+  unsigned long long* argmax_keys;
 };
 int gemv_splits(int N, int K);
 size_t gemv_partial_floats(int B, int N, int K);
@@ -89,10 +93,19 @@ hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* 
 template <typename T>
 hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0,
                        T* vt, int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s);
-// Decode: qkv fp32 [B, (n_q+2n_kv)D]; rotate at pos[b]; q -> qout [B, n_q, D]; k, v -> paged cache.
+// Decode: qkv = sum over `splits` fp32 slabs [splits][B][(n_q+2n_kv)D] (1 slab: the projection
+// itself); rotate at pos[b]; q -> qout [B, n_q, D]; k, v -> paged cache.
 template <typename T>
-hipError_t qkv_decode(const float* qkv, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos,
+hipError_t qkv_decode(const float* qkv, int splits, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos,
                       T* qout, T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s);
+// Decode residual + RMSNorm, one workgroup per row: x[b] += sum_s partial[s][b] (if splits > 0),
+// then a[b] = x[b] / sqrt(mean(x[b]^2) + eps) * g.
+// keys != null: also zero keys[b] for the fused argmax of the projection that follows.
+template <typename T>
+hipError_t resid_rmsnorm(const float* partial, int splits, float* x, int B, int H, const bf16_t* g, float eps, T* a,
+                         int lda, unsigned long long* keys, hipStream_t s);
+// ids[b] = the token id packed in keys[b] by the fused argmax.
+hipError_t argmax_finish(const unsigned long long* keys, int B, int* ids, hipStream_t s);
 // x[r] = r < n_vis ? vis[r] : embed[ids[r - n_vis]]  (fp32 out)
 template <typename T>
 hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const bf16_t* embed, int H, float* x,

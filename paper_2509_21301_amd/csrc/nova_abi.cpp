@@ -514,8 +514,7 @@ size_t prefill_ws(const nova_llm* m, int S, Carve* cv) {
   w.take<T>((size_t)c.n_kv * c.head_dim * round_up(S, 64));      // V^T
   w.take<T>((size_t)S * c.n_q * c.head_dim);                     // attention out
   w.take<T>((size_t)S * m->ip);                                  // MLP hidden
-  w.take<float>((size_t)c.vocab);                                // logits
-  w.take<float>(nova::gemv_partial_floats(1, c.vocab, c.hidden));
+  w.take<unsigned long long>(1);                                 // argmax key
   return w.used;
 }
 template <typename T>
@@ -530,7 +529,7 @@ size_t decode_ws(const nova_llm* m, int B, int max_ctx, Carve* cv) {
   w.take<T>((size_t)B * c.n_q * c.head_dim);            // rotated q
   w.take<T>((size_t)B * c.n_q * c.head_dim);            // attention out
   w.take<T>((size_t)B * m->ip);                         // MLP hidden
-  w.take<float>((size_t)B * c.vocab);                   // logits
+  w.take<unsigned long long>((size_t)B);                // argmax keys
   size_t part = 0;
   const int qd = c.n_q * c.head_dim;
   part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden));
@@ -568,9 +567,7 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
   T* vt = w.take<T>((size_t)c.n_kv * D * skp);
   T* att = w.take<T>((size_t)S * qd);
   T* hm = w.take<T>((size_t)S * m->ip);
-  float* logits = w.take<float>(c.vocab);
-  float* part = w.take<float>(nova::gemv_partial_floats(1, c.vocab, H));
-  if (logits_out) logits = logits_out;
+  unsigned long long* keys = w.take<unsigned long long>(1);
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
 
   CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(vis, n_vis, ids, n_text, (const bf16_t*)m->d.embed, H, x, s));
@@ -604,13 +601,13 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
     }
   }
   const char* hw = (const char*)m->d.head;
-  CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x + (size_t)(S - 1) * H, 1, H, (const bf16_t*)(hw + m->head.off[0]), nullptr,
-                                             c.eps, 0, a, H, 1, 0, 0, s));
+  CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, x + (size_t)(S - 1) * H, 1, H,
+                                                 (const bf16_t*)(hw + m->head.off[0]), c.eps, a, H, keys, s));
   {
-    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, 1, c.vocab, H, logits, c.vocab, part};
-    CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
+    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, 1, c.vocab, H, logits_out, c.vocab, nullptr, keys};
+    CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
-  CALL(NOVA_KIND_MISC, s, nova::argmax_rows(logits, 1, c.vocab, next_id, s));
+  CALL(NOVA_KIND_MISC, s, nova::argmax_finish(keys, 1, next_id, s));
   return NOVA_OK;
 }
 
@@ -626,7 +623,7 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
   T* q = w.take<T>((size_t)B * qd);
   T* att = w.take<T>((size_t)B * qd);
   T* hm = w.take<T>((size_t)B * m->ip);
-  float* logits = w.take<float>((size_t)B * c.vocab);
+  unsigned long long* keys = w.take<unsigned long long>((size_t)B);
   size_t partn = 0;
   partn = std::max(partn, nova::gemv_partial_floats(B, m->qkvw, H));
   partn = std::max(partn, nova::gemv_partial_floats(B, H, qd));
@@ -635,46 +632,60 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
   partn = std::max(partn, nova::gemv_partial_floats(B, c.vocab, H));
   float* part = w.take<float>(partn);
   float* apart = w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, D, max_ctx, c.n_kv));
-  if (logits_out) logits = logits_out;
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
 
+  // Split-K projections leave their partials for the next kernel: the QKV partials are summed by
+  // the rotary/KV-append kernel, the O and down partials by the fused residual + RMSNorm.
+  const int sp_qkv = nova::gemv_splits(m->qkvw, H);
+  const int sp_o = nova::gemv_splits(H, qd);
+  const int sp_down = nova::gemv_splits(H, m->ip);
+  const char* hw = (const char*)m->d.head;
+  auto layer_w = [&](int l, int i) {
+    return (const bf16_t*)((const char*)m->d.layers + (size_t)l * m->lay.bytes + m->lay.off[i]);
+  };
   CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(nullptr, 0, ids, B, (const bf16_t*)m->d.embed, H, x, s));
+  if (c.layers > 0)
+    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, x, B, H, layer_w(0, 0), c.eps, a, H, nullptr, s));
+  else
+    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, x, B, H, (const bf16_t*)(hw + m->head.off[0]), c.eps, a, H,
+                                                   keys, s));
   for (int l = 0; l < c.layers; ++l) {
-    const char* lw = (const char*)m->d.layers + (size_t)l * m->lay.bytes;
-    auto W = [&](int i) { return (const bf16_t*)(lw + m->lay.off[i]); };
+    auto W = [&](int i) { return layer_w(l, i); };
+    const bf16_t* next_gain = l + 1 < c.layers ? layer_w(l + 1, 0) : (const bf16_t*)(hw + m->head.off[0]);
     T* kp = (T*)kv->k + l * kv_layer;
     T* vp = (T*)kv->v + l * kv_layer;
-    CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, B, H, W(0), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
     {
-      GemvArgs p{a, H, W(1), H, B, m->qkvw, H, qkv, m->qkvw, part};
+      GemvArgs p{a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : qkv, m->qkvw, part, nullptr};
       CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
     }
-    CALL(NOVA_KIND_MISC, s, nova::qkv_decode<T>(qkv, B, c.n_q, c.n_kv, D, c.rope_theta, pos, q, kp, vp, tables, max_blocks, c.block, s));
+    CALL(NOVA_KIND_MISC, s, nova::qkv_decode<T>(sp_qkv > 1 ? part : qkv, sp_qkv, B, c.n_q, c.n_kv, D, c.rope_theta, pos, q,
+                                                 kp, vp, tables, max_blocks, c.block, s));
     {
       nova::DecAttnArgs p{q, kp, vp, tables, max_blocks, pos, att, apart, B, c.n_q, c.n_kv, c.block, max_ctx};
       CALL(NOVA_KIND_DECODE_ATTN, s, nova::decode_attention<T>(p, D, s));
     }
     {
-      GemvArgs p{att, qd, W(2), qd, B, H, qd, x, H, part};
+      GemvArgs p{att, qd, W(2), qd, B, H, qd, sp_o > 1 ? nullptr : x, H, part, nullptr};
       CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
     }
-    CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, B, H, W(3), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
+    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_o > 1 ? part : nullptr, sp_o > 1 ? sp_o : 0, x, B, H, W(3), c.eps, a, H,
+                                                   nullptr, s));
     {
-      GemvArgs p{a, H, W(4), H, B, 2 * m->ip, H, hm, m->ip, part};
+      GemvArgs p{a, H, W(4), H, B, 2 * m->ip, H, hm, m->ip, part, nullptr};
       CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
     }
     {
-      GemvArgs p{hm, m->ip, W(5), m->ip, B, H, m->ip, x, H, part};
+      GemvArgs p{hm, m->ip, W(5), m->ip, B, H, m->ip, sp_down > 1 ? nullptr : x, H, part, nullptr};
       CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
     }
+    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_down > 1 ? part : nullptr, sp_down > 1 ? sp_down : 0, x, B, H,
+                                                   next_gain, c.eps, a, H, l + 1 < c.layers ? nullptr : keys, s));
   }
-  const char* hw = (const char*)m->d.head;
-  CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, B, H, (const bf16_t*)(hw + m->head.off[0]), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
   {
-    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits, c.vocab, part};
-    CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
+    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, nullptr, keys};
+    CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
-  CALL(NOVA_KIND_MISC, s, nova::argmax_rows(logits, B, c.vocab, next_ids, s));
+  CALL(NOVA_KIND_MISC, s, nova::argmax_finish(keys, B, next_ids, s));
   return NOVA_OK;
 }
 }  // namespace

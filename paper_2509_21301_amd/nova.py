@@ -231,13 +231,13 @@ def pack_llm(cfg, w, act=ACT_BF16, device="cuda"):
         _put(lay, base + lo[1], qkv, ((cfg.n_q + 2 * cfg.n_kv) * d, H), device)
         _put(lay, base + lo[2], w[p + "o.w"], (H, cfg.n_q * d), device)
         _put(lay, base + lo[3], w[p + "rms2.g"], (H,), device)
-        gu = lay.view(base + lo[4], (I // 16, 2, 16, H))
+        gu = lay.view(base + lo[4], (I // 8, 2, 8, H))
         gate = torch.zeros(I, H, dtype=torch.bfloat16, device=gu.device)
         up = torch.zeros(I, H, dtype=torch.bfloat16, device=gu.device)
         gate[: cfg.inter] = _bf16(w[p + "gate.w"], gu.device)
         up[: cfg.inter] = _bf16(w[p + "up.w"], gu.device)
-        gu[:, 0].copy_(gate.view(I // 16, 16, H))
-        gu[:, 1].copy_(up.view(I // 16, 16, H))
+        gu[:, 0].copy_(gate.view(I // 8, 8, H))
+        gu[:, 1].copy_(up.view(I // 8, 8, H))
         _put(lay, base + lo[5], w[p + "down.w"], (H, I), device)
     head = _Blob(hb, device)
     _put(head, ho[0], w["norm.g"], (H,), device)
