@@ -209,6 +209,11 @@ int nova_make_cu_mask(int n_cus, int first_slot, uint32_t* mask);
  * An empty mask, a mask with no CU on some XCD, or stage out of range gives NOVA_EINVAL. */
 int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int mask_words, nova_stream_t* out_stream);
 
+/* Diagnostic: launch n_workgroups single-wave workgroups on `stream`; workgroup i writes
+ * (xcd << 16) | (shader_engine << 8) | cu of the compute unit it ran on into out[i]
+ * (device uint32 [n_workgroups]).  Used to check that a partition stream stays on its CUs. */
+int nova_cu_probe(nova_stream_t stream, uint32_t* out, int n_workgroups);
+
 /* ------------------------------------------------------------------ kernel timing
  * When on, every kernel family launch inside the stage calls is bracketed by HIP events on
  * its stream.  nova_timing_read waits for the recorded events of `kind` (NOVA_KIND_*), returns

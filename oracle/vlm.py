@@ -178,6 +178,26 @@ def vit_encode(img, w, cfg, layers=None):
     return merge_adapter(x, w, cfg)
 
 
+def vit_encode_tokens(img, w, cfg, tokens):
+    """Vision encode evaluated only at the merged output ``tokens`` (row-major over the merged grid).
+
+    Every layer but the last runs on all patches; the last one only at the patches the
+    requested tokens merge ((2i,2j), (2i,2j+1), (2i+1,2j), (2i+1,2j+1) for token (i, j)), with
+    keys and values from all patches.  Returns [len(tokens), out_hidden].
+    """
+    x = patch_embed(img, w, cfg)
+    for l in range(cfg.layers - 1):
+        x = vit_layer(x, w, l, cfg)
+    m, gw = cfg.merge, cfg.grid_w
+    rows = []
+    for t in tokens:
+        i, j = divmod(int(t), gw // m)
+        rows += [(m * i + dy) * gw + (m * j + dx) for dy in range(m) for dx in range(m)]
+    y = vit_layer(x, w, cfg.layers - 1, cfg, rows=np.array(rows)) if cfg.layers > 0 else x[np.array(rows)]
+    a = layer_norm(y, w["merge.ln.g"], w["merge.ln.b"], cfg.eps).reshape(len(tokens), m * m * cfg.hidden)
+    return linear(a, w["merge.w"], w["merge.b"])
+
+
 # --------------------------------------------------------------------------------------
 # paged KV cache
 # --------------------------------------------------------------------------------------

@@ -308,6 +308,27 @@ hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ CU placement probe
+__global__ void cu_probe_kernel(uint32_t* __restrict__ out, int n) {
+  if (threadIdx.x == 0 && (int)blockIdx.x < n) {
+    uint32_t hw, xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const uint32_t cu = (hw >> 8) & 0xfu, se = (hw >> 13) & 0x7u;
+    out[blockIdx.x] = ((xcc & 0xfu) << 16) | (se << 8) | cu;
+  }
+  // keep each workgroup resident briefly so that the dispatcher spreads them over all CUs
+  const long long t0 = clock64();
+  while (clock64() - t0 < 20000) {
+  }
+}
+
+hipError_t cu_probe(hipStream_t s, uint32_t* out, int n) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(cu_probe_kernel, dim3(n), dim3(64), 0, s, out, n);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ greedy argmax (ties -> lowest index)
 __global__ void argmax_kernel(const float* __restrict__ logits, int V, int* __restrict__ out) {
   const float* row = logits + (size_t)blockIdx.x * V;

@@ -111,5 +111,6 @@ template <typename T>
 hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const bf16_t* embed, int H, float* x,
                       hipStream_t s);
 hipError_t argmax_rows(const float* logits, int B, int V, int* out, hipStream_t s);
+hipError_t cu_probe(hipStream_t s, uint32_t* out, int n);
 
 }  // namespace nova

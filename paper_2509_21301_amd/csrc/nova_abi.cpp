@@ -775,6 +775,12 @@ extern "C" int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int 
   return NOVA_OK;
 }
 
+extern "C" int nova_cu_probe(nova_stream_t stream, uint32_t* out, int n) {
+  if (!out || n <= 0) return fail(NOVA_EINVAL, "cu_probe needs an output array and n > 0");
+  HIP_TRY(nova::cu_probe((hipStream_t)stream, out, n));
+  return NOVA_OK;
+}
+
 // ------------------------------------------------------------------ timing
 extern "C" int nova_timing_enable(int on) {
   g.timing = on != 0;

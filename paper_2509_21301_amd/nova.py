@@ -81,6 +81,7 @@ _SIG = {
                                   C.POINTER(KvC), C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "nova_make_cu_mask": (C.c_int, [C.c_int, C.c_int, C.POINTER(C.c_uint32)]),
     "nova_set_stage_partition": (C.c_int, [C.c_int, C.POINTER(C.c_uint32), C.c_int, C.POINTER(C.c_void_p)]),
+    "nova_cu_probe": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int]),
     "nova_timing_enable": (C.c_int, [C.c_int]),
     "nova_timing_read": (C.c_int, [C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int)]),
 }
@@ -377,6 +378,16 @@ def set_stage_partition(stage: int, mask) -> torch.cuda.ExternalStream:
     s = C.c_void_p()
     _check(lib.nova_set_stage_partition(stage, arr, len(mask), C.byref(s)))
     return torch.cuda.ExternalStream(s.value)
+
+
+def cu_probe(stream, n_workgroups: int = 4096):
+    """(xcd, shader engine, cu) of the CU each probe workgroup ran on, as a set."""
+    out = torch.zeros(n_workgroups, dtype=torch.int32, device="cuda")
+    _check(lib.nova_cu_probe(_stream(stream), _ptr(out), n_workgroups))
+    stream = stream or torch.cuda.current_stream()
+    stream.synchronize()
+    v = out.cpu().numpy().astype(np.uint32)
+    return {(int(x >> 16), int((x >> 8) & 0xff), int(x & 0xff)) for x in v}
 
 
 def timing_enable(on: bool = True):

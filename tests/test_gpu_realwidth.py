@@ -1,0 +1,107 @@
+"""Parity at the real model widths and sequence lengths, on sampled outputs the oracle computes
+one by one (through the C ABI, bf16, tolerance 2e-2):
+
+* vision encode: one 1280-wide layer (16 heads of 80, MLP 5120) on two 1008x1008 images
+  (5184 patches each) with the 2x2 merge to 3584 -- sampled merged tokens of both images;
+* prefill: one 3584-wide GQA layer (28/4 heads of 128, SwiGLU 18944, vocab 152064) over
+  1300 visual embeddings + 200 text tokens -- last-row logits, greedy id, sampled K/V;
+* decode: 20 sequences with ragged contexts of 1200..1500 tokens in a shuffled paged cache
+  (random bf16 K/V shared with the oracle) -- logits of every sequence and the appended K/V.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import vlm
+from paper_2509_21301_amd import synth
+from tests import stage_cases as sc
+
+pytestmark = pytest.mark.gpu
+
+VIT1 = dataclasses.replace(synth.VIT_1008, layers=1)
+LLM1 = dataclasses.replace(synth.LLM_28, layers=1)
+
+
+def test_vit_layer_real_width(gpu_lib):
+    import torch
+    nova = gpu_lib
+    w = synth.vit_weights(VIT1, seed=0)
+    imgs = synth.image(2, VIT1.image_h, VIT1.image_w, seed=1)
+    out = nova.Vit(VIT1, w).encode(torch.from_numpy(imgs).cuda().to(torch.bfloat16)).float().cpu().numpy()
+    tokens = [0, 35, 36, 647, 1259, 1295]          # corners, row ends, the middle of the 36x36 grid
+    for i in range(2):
+        ref = vlm.vit_encode_tokens(imgs[i], w, VIT1, tokens)
+        assert vlm.max_rel_err(out[i, tokens], ref) < sc.TOL_BF16, f"image {i}"
+
+
+@pytest.fixture(scope="module")
+def llm1():
+    import torch
+    from paper_2509_21301_amd import nova
+    w = synth.llm_weights(LLM1, seed=0)
+    return w, nova.Llm(LLM1, w)
+
+
+def test_prefill_layer_real_width(gpu_lib, llm1):
+    import torch
+    nova = gpu_lib
+    w, llm = llm1
+    nv, nt = synth.LLM_VISION_TOKENS, synth.LLM_TEXT_TOKENS
+    vis = synth.vision_embeds(nv, LLM1.hidden)
+    ids = synth.text_ids(nt, LLM1.vocab)
+    s = nv + nt
+    table, pool = synth.block_tables([s], LLM1.block, seed=5)
+    kv = nova.KvPool(llm, pool)
+    logits = torch.empty(LLM1.vocab, dtype=torch.float32, device="cuda")
+    nxt = llm.prefill(torch.from_numpy(vis).cuda().to(torch.bfloat16), torch.from_numpy(ids).cuda(),
+                      torch.from_numpy(table[0]).cuda(), kv, logits=logits)
+    torch.cuda.synchronize()
+    x = np.concatenate([vis, w["embed"][ids]], 0)
+    rows = np.array([0, 777, 1299, 1300, s - 1])
+    hid, k, v = vlm.llm_layer_rows(x, w, 0, LLM1, rows)
+    ref_logits = vlm.lm_head(hid[-1:], w, LLM1)[0]
+    got = logits.cpu().numpy()
+    assert vlm.max_rel_err(got, ref_logits) < sc.TOL_BF16
+    top = np.sort(ref_logits)[::-1]
+    if top[0] - top[1] > 2 * np.abs(got - ref_logits).max():
+        assert int(nxt.item()) == int(np.argmax(ref_logits))
+    k5 = kv.k5.float().cpu().numpy()
+    v5 = kv.v5.float().cpu().numpy()
+    for p in [0, 15, 16, 1000, s - 1]:
+        blk, slot = table[0][p // 16], p % 16
+        assert vlm.max_rel_err(k5[0, blk, :, slot, :], k[p]) < sc.TOL_BF16
+        assert vlm.max_rel_err(v5[0, blk, :, :, slot], v[p]) < sc.TOL_BF16
+
+
+def test_decode_batch20_real_width(gpu_lib, llm1):
+    import torch
+    nova = gpu_lib
+    w, llm = llm1
+    cfg = LLM1
+    bsz = 20
+    ctx = [1500 - 15 * b for b in range(bsz)]                    # positions of the new tokens
+    tables, pool = synth.block_tables([c + 1 for c in ctx], cfg.block, seed=9)
+    rng = np.random.default_rng(3)
+    kref = vlm.PagedKV(cfg.layers, pool, cfg.n_kv, cfg.block, cfg.head_dim)
+    kref.k[:] = synth.bf16_round(rng.standard_normal(kref.k.shape, dtype=np.float32))
+    kref.v[:] = synth.bf16_round(rng.standard_normal(kref.v.shape, dtype=np.float32))
+    kv = nova.KvPool(llm, pool)
+    kv.k5.copy_(torch.from_numpy(kref.k.astype(np.float32)).to(torch.bfloat16))
+    kv.v5.copy_(torch.from_numpy(np.swapaxes(kref.v, -1, -2).astype(np.float32)).to(torch.bfloat16))
+    ids = synth.text_ids(bsz, cfg.vocab, seed=12)
+    pos = np.array(ctx, np.int32)
+    logits = torch.empty(bsz, cfg.vocab, dtype=torch.float32, device="cuda")
+    nxt = llm.decode(torch.from_numpy(ids).cuda(), torch.from_numpy(pos).cuda(), torch.from_numpy(tables).cuda(),
+                     kv, max_ctx=max(ctx) + 1, logits=logits)
+    torch.cuda.synchronize()
+    ref_logits, ref_ids = vlm.llm_decode_step(ids, pos, tables, kref, w, cfg)
+    got = logits.cpu().numpy()
+    got_ids = nxt.cpu().numpy()
+    for b in range(bsz):
+        assert vlm.max_rel_err(got[b], ref_logits[b]) < sc.TOL_BF16, f"seq {b}"
+        top = np.sort(ref_logits[b])[::-1]
+        if top[0] - top[1] > 2 * np.abs(got[b] - ref_logits[b]).max():
+            assert got_ids[b] == ref_ids[b], f"seq {b}"
+    ek, ev = sc.kv_errors(kref.k, kref.v, kv.k5.float().cpu().numpy(), kv.v5.float().cpu().numpy())
+    assert ek < sc.TOL_BF16 and ev < sc.TOL_BF16

@@ -207,6 +207,16 @@ def test_vit_layer_permutation_equivariant_and_rows():
     assert np.allclose(vlm.vit_layer(x, w, 0, cfg, rows=rows), a[rows], atol=1e-12)
 
 
+def test_vit_encode_tokens_equals_full_encode():
+    cfg = synth.VitConfig(hidden=64, heads=2, mlp=96, layers=2, patch=2, merge=2, out_hidden=64,
+                          image_h=8, image_w=12)
+    w = synth.vit_weights(cfg, seed=5)
+    img = synth.image(1, 8, 12, seed=5)[0]
+    full = vlm.vit_encode(img, w, cfg)
+    toks = [0, 4, 5]
+    assert np.allclose(vlm.vit_encode_tokens(img, w, cfg, toks), full[toks], atol=1e-12)
+
+
 # ----------------------------------------------------------------------------- LLM
 def _hf_llama(w, cfg):
     from transformers import LlamaConfig, LlamaForCausalLM
