@@ -168,6 +168,41 @@ class Stages:
                         next_ids=self.next_ids[:batch], stream=stream)
 
 
+class ServingSetup:
+    """The screenshot workload: a 1092x2408 image (13416 patches, 3354 merged tokens) through the
+    same 32-layer encoder (its own position table), prompts of 3354 + 150..300 tokens."""
+
+    def __init__(self, nova, torch, synth, st):
+        self.nova, self.torch, self.synth, self.st = nova, torch, synth, st
+        cfg = synth.VIT_SCREEN
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(11)
+        (eo, eb), _, _ = nova.vit_layouts(cfg)
+        emb = random_blob(eb, eo, [], "cuda", gen)
+        self.vit = nova.Vit(cfg, None, blobs=(emb, st.vit.layers, st.vit.head, st.vit.layer_bytes))
+        img = synth.image(1, cfg.image_h, cfg.image_w, seed=21)
+        self.pixels = torch.from_numpy(img).to("cuda", torch.bfloat16).contiguous()
+        self.vis = torch.empty(self.vit.out_shape(1), dtype=torch.bfloat16, device="cuda")
+        nt = 225
+        self.ids = torch.from_numpy(synth.text_ids(nt, st.lc.vocab, seed=22)).cuda()
+        s = cfg.n_out + nt
+        self.max_blocks = (cfg.n_out + 300 + 48 + 15) // 16
+        tables, pool = synth.block_tables([s], 16, seed=23, num_blocks=12000)
+        self.kv = nova.KvPool(st.llm, pool)
+        self.table = torch.from_numpy(tables[0]).cuda()
+
+    def encode(self, stream):
+        self.vit.encode(self.pixels, out=self.vis, stream=stream)
+
+    def prefill(self, stream):
+        self.st.llm.prefill(self.vis[0], self.ids, self.table, self.kv, stream=stream)
+
+    def serve(self, kw, trace):
+        from paper_2509_21301_amd import serve
+        srv = serve.Server(self.vit, self.st.llm, self.kv, self.pixels, max_blocks=self.max_blocks, **kw)
+        return srv.run(trace)
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 def cpu_baseline(synth):
     """The oracle, as is, on one image's worth of encoder layers at the real shape (2 of 32
@@ -210,6 +245,8 @@ def main():
     ap.add_argument("--batch", type=int, default=8, help="images per encode pass (headline)")
     ap.add_argument("--no-sweep", action="store_true", help="skip CU-share curves and co-run")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--rates", type=float, nargs="+", default=[4.0], help="request rates (req/s) of the serving runs")
+    ap.add_argument("--window", type=float, default=10.0, help="arrival window (s) of each serving run")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
     ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32"],
                     help="run only this stage in a loop of --steps passes (for rocprofv3)")
@@ -220,7 +257,7 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2509_21301_amd import nova, synth
+    from paper_2509_21301_amd import nova, sched, serve, synth
     device = "cuda"
     nova.init(0)
     st = Stages(nova, torch, synth, device, args.batch)
@@ -330,17 +367,19 @@ def main():
             curves["decode_b8_tok_per_s"].append(round(8 / (ms_d / 1e3), 1))
             log(f"share {p:3d} CUs: encode {ms_e:.2f} ms, prefill {ms_p:.2f} ms, decode(b8) {ms_d:.3f} ms")
         result["cu_share_curves"] = curves
-        # co-run: decode (batch 8) on P CUs with encode (batch 1) or prefill on the other 256 - P
+        # co-run on the serving shapes: decode (batch 8) on P CUs with the screenshot encode or a
+        # 3.5k-token prefill on the other 256 - P; these are the curves the Eq. 3 search consumes
+        srv = ServingSetup(nova, torch, synth, st)
         corun = []
         for other in ("encode", "prefill"):
             for p in [32, 64, 96, 128, 160, 192, 224]:
                 s_d = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(p, 0))
                 so = nova.set_stage_partition(nova.STAGE_ENCODE if other == "encode" else nova.STAGE_PREFILL,
                                               nova.make_cu_mask(256 - p, p // 8))
-                run_other = (lambda: st.encode(1, stream=so)) if other == "encode" else (lambda: st.prefill(stream=so))
-                torch.cuda.synchronize()
-                t_o = time_passes(torch, run_other, 1, so)          # solo on its partition (warm)
-                n_dec = 40
+                run_other = (lambda: srv.encode(so)) if other == "encode" else (lambda: srv.prefill(so))
+                t_o = time_passes(torch, run_other, 1, so)
+                t_d = time_passes(torch, lambda: st.decode(8, stream=s_d), 5, s_d)
+                n_dec = max(4, int(t_o / max(t_d, 1e-3)) + 2)
                 torch.cuda.synchronize()
                 eo0, eo1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 ed0, ed1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -356,9 +395,33 @@ def main():
                 t_dc = ed0.elapsed_time(ed1) / n_dec
                 corun.append({"pair": f"decode+{other}", "decode_cus": p, "other_cus": 256 - p,
                               f"{other}_ms_solo_on_partition": round(t_o, 3), f"{other}_ms_corun": round(t_oc, 3),
-                              "decode_step_ms_corun": round(t_dc, 3)})
-                log(f"co-run decode {p} / {other} {256 - p}: {other} {t_oc:.2f} ms (solo {t_o:.2f}), decode step {t_dc:.3f} ms")
+                              "decode_step_ms_solo_on_partition": round(t_d, 3), "decode_step_ms_corun": round(t_dc, 3)})
+                log(f"co-run decode {p} / {other} {256 - p}: {other} {t_oc:.2f} ms (solo {t_o:.2f}), "
+                    f"decode step {t_dc:.3f} ms (solo {t_d:.3f})")
         result["corun"] = corun
+        curves = sched.StageCurves.from_corun(corun)
+        out_len = 32.0                                   # mean of the U{16..48} output lengths
+        pv, pp, lat = sched.best_static(curves, out_len)
+        result["static_optimum"] = {"decode_cus_with_encode": pv, "decode_cus_with_prefill": pp,
+                                    "expected_e2e_s": round(lat, 4), "mean_output_tokens": out_len,
+                                    "ideal_req_per_s": round(sched.ideal_throughput(curves, pv, pp), 3)}
+        result["pareto_front"] = [{"e2e_s": round(a, 4), "req_per_s": round(b, 3), "decode_cus_with_encode": c,
+                                   "decode_cus_with_prefill": d} for a, b, c, d in sched.pareto_front(curves, out_len)]
+        log(f"Eq. 3 optimum: decode {pv} CUs beside encode, {pp} beside prefill, expected E2E {lat:.3f} s")
+        # serving: Poisson bursts through the Alg. 1 policy, co-run partitions vs time slicing
+        serving = []
+        for rate in args.rates:
+            for mode, kw in [("nova_static", dict(mode="nova", decode_cus=(pv, pp))),
+                             ("nova_adaptive", dict(mode="nova", decode_cus=(pv, pp), alpha=32, minimum=32)),
+                             ("time_sliced", dict(mode="time_sliced")),
+                             ("multi_stream", dict(mode="multi_stream"))]:
+                trace = serve.poisson_trace(rate, args.window, seed=3)
+                res = srv.serve(kw, trace)
+                res.update({"mode": mode, "rate_req_s": rate, "window_s": args.window})
+                serving.append(res)
+                log(f"serve {mode:13s} rate {rate}: max E2E {res['max_e2e_s']:.3f} s, avg {res['avg_e2e_s']:.3f} s, "
+                    f"avg TBT {res['avg_tbt_ms']:.1f} ms, {res['throughput_req_s']:.2f} req/s")
+        result["serving"] = serving
 
     if not args.no_cpu:
         log("timing the oracle on the host (bounded sample)")

@@ -1,0 +1,83 @@
+"""Partition planning for co-running stages (the paper's Sec. 3.3): expected end-to-end latency
+of an ideal pipeline (Eq. 1-2), the enumeration of the best static partition (Eq. 3), the
+throughput approximation (Eq. 4), the latency-throughput Pareto front, and the adaptive decode
+share (Eq. 5), all driven by measured per-stage curves.
+
+A partition here is the number of CUs the decode stage holds while it co-runs with vision
+encode (P_v) or with prefill (P_p); the co-running stage holds the rest of the 256.  On
+gfx950 a partition is a whole number of XCD-balanced mask groups (8 CUs = one per XCD).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+TOTAL_CUS = 256
+GRANULE = 8
+
+
+@dataclass
+class StageCurves:
+    """Measured co-run times (seconds) indexed by the decode CU count."""
+    shares: list[int]
+    t_vision: dict[int, float]          # encode pass while decode holds the share
+    t_prefill: dict[int, float]         # prefill pass while decode holds the share
+    t_dec_vision: dict[int, float]      # decode step while co-running with encode
+    t_dec_prefill: dict[int, float]     # decode step while co-running with prefill
+
+    @classmethod
+    def from_corun(cls, records):
+        """Build from bench.py's `corun` records (milliseconds)."""
+        tv, tp, dv, dp, shares = {}, {}, {}, {}, set()
+        for r in records:
+            p = r["decode_cus"]
+            shares.add(p)
+            if r["pair"] == "decode+encode":
+                tv[p] = r["encode_ms_corun"] / 1e3
+                dv[p] = r["decode_step_ms_corun"] / 1e3
+            else:
+                tp[p] = r["prefill_ms_corun"] / 1e3
+                dp[p] = r["decode_step_ms_corun"] / 1e3
+        return cls(sorted(shares), tv, tp, dv, dp)
+
+
+def expected_e2e(c: StageCurves, pv: int, pp: int, out_len: float) -> float:
+    """Eq. 1 with the co-run proportions of Eq. 2."""
+    tv, tp = c.t_vision[pv], c.t_prefill[pp]
+    share_v = tv / (tv + tp)
+    return tv + tp + (share_v * c.t_dec_vision[pv] + (1.0 - share_v) * c.t_dec_prefill[pp]) * out_len
+
+
+def ideal_throughput(c: StageCurves, pv: int, pp: int) -> float:
+    """Eq. 4: requests per second when encode and prefill run back to back."""
+    return 1.0 / (c.t_vision[pv] + c.t_prefill[pp])
+
+
+def best_static(c: StageCurves, out_len: float):
+    """Eq. 3: (P_v, P_p, latency) minimising Eq. 1 over all measured partition pairs."""
+    best = None
+    for pv in c.shares:
+        for pp in c.shares:
+            lat = expected_e2e(c, pv, pp, out_len)
+            if best is None or lat < best[2]:
+                best = (pv, pp, lat)
+    return best
+
+
+def pareto_front(c: StageCurves, out_len: float):
+    """Partition pairs whose (latency, throughput) no other pair improves on both counts.
+    Returns [(latency, throughput, P_v, P_p)] sorted by latency."""
+    pts = [(expected_e2e(c, a, b, out_len), ideal_throughput(c, a, b), a, b) for a in c.shares for b in c.shares]
+    pts.sort(key=lambda t: (t[0], -t[1]))
+    front, best_thr = [], -1.0
+    for p in pts:
+        if p[1] > best_thr:
+            front.append(p)
+            best_thr = p[1]
+    return front
+
+
+def decode_cus(n_pending: int, optimum: int, alpha: int, minimum: int, granule: int = GRANULE) -> int:
+    """Eq. 5: decode's CUs shrink by alpha per pending encode/prefill request beyond the first,
+    never below the floor; rounded down to the mask granule."""
+    cus = max(minimum, optimum - alpha * (max(n_pending, 1) - 1))
+    return max(granule, cus // granule * granule)

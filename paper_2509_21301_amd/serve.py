@@ -1,0 +1,330 @@
+"""Co-run serving driver: requests (screenshot + instruction) flow through vision encode,
+prefill and in-flight-batched decode on one GPU, scheduled by the policy of the paper's Alg. 1.
+
+Policy (Sec. 3.4): FIFO within a stage; decode has the highest priority and co-runs with vision
+encode or prefill on disjoint CU partitions; vision encode and prefill never run together, and
+prefill goes before vision; decode requests join the running batch at the next step (in-flight
+batching); partitions change only at forward-pass boundaries.  Partition modes:
+
+* ``nova``         -- decode holds P CUs while co-running, the other stage 256 - P (static P,
+                      or Eq. 5 from the number of requests in vision/prefill);
+* ``multi_stream`` -- the same worker threads on unrestricted streams (the paper's Multi-Stream);
+* ``time_sliced``  -- one worker runs one forward pass at a time on the whole GPU, alternating a
+                      decode step with each encode/prefill pass.
+
+Every worker is a thread that enqueues its pass on its stream through the C ABI and waits for
+it; the scheduler thread owns the request state.  All timing is wall clock.
+"""
+from __future__ import annotations
+
+import queue
+import threading
+import time
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import nova, sched, synth
+
+FULL = [0xFFFFFFFF] * 8
+
+
+@dataclass
+class Request:
+    rid: int
+    arrival: float                 # seconds after the trace start
+    n_text: int
+    n_out: int
+    ids: torch.Tensor = None
+    table_row: np.ndarray = None
+    blocks: list = field(default_factory=list)
+    t_arrive: float = 0.0
+    t_vis0: float = 0.0
+    t_vis1: float = 0.0
+    t_pre1: float = 0.0
+    t_tokens: list = field(default_factory=list)
+    last_token: int = 0
+
+    @property
+    def done(self):
+        return len(self.t_tokens) >= self.n_out
+
+
+def poisson_trace(rate, window_s, seed, n_text=(150, 300), n_out=(16, 48)):
+    """Poisson(rate) arrivals over one window; text length and output length uniform (inclusive)."""
+    r = np.random.default_rng([seed, int(rate * 1000)])
+    t, out = 0.0, []
+    while True:
+        t += r.exponential(1.0 / rate)
+        if t >= window_s:
+            break
+        out.append(Request(len(out), t, int(r.integers(n_text[0], n_text[1] + 1)), int(r.integers(n_out[0], n_out[1] + 1))))
+    return out
+
+
+class BlockPool:
+    """Host free list of paged-KV blocks."""
+
+    def __init__(self, n):
+        self.free = list(range(n))[::-1]
+        self.lock = threading.Lock()
+
+    def take(self, n):
+        with self.lock:
+            if len(self.free) < n:
+                raise nova.NovaError(nova.ENOKV, f"KV pool exhausted ({n} blocks wanted, {len(self.free)} free)")
+            return [self.free.pop() for _ in range(n)]
+
+    def give(self, blocks):
+        with self.lock:
+            self.free.extend(blocks)
+
+
+class Server:
+    def __init__(self, vit, llm, kv, pixels, mode="nova", decode_cus=(96, 96), alpha=0, minimum=32, max_batch=32,
+                 max_blocks=256, device="cuda"):
+        """decode_cus = (P_v, P_p): decode's CUs while co-running with vision encode / prefill
+        (Eq. 3's optimum); alpha > 0 turns on the Eq. 5 adaptation with floor `minimum`."""
+        self.vit, self.llm, self.kv, self.pixels, self.device = vit, llm, kv, pixels, device
+        self.mode, self.decode_cus, self.alpha, self.minimum = mode, decode_cus, alpha, minimum
+        self.other = None             # stage co-running with decode: STAGE_ENCODE, STAGE_PREFILL or None
+        self.max_batch, self.max_blocks = max_batch, max_blocks
+        self.cfg = llm.cfg
+        self.blocks = BlockPool(kv.num_blocks)
+        self.n_vis = vit.cfg.n_out
+        self.vis_buf = torch.empty(1, self.n_vis, self.cfg.hidden, dtype=torch.bfloat16, device=device)
+        self.events = queue.Queue()
+        self.lock = threading.Lock()
+        self.n_pending = 0            # requests queued for or inside vision encode / prefill
+        self.decode_active = 0        # requests in the decode batch or waiting to join it
+        self.partition_log = []
+
+    # ---------------------------------------------------------------- partitions
+    def _masks(self, stage):
+        """Mask for `stage` at a pass boundary, from the current load (Eq. 5 when alpha > 0)."""
+        if self.mode != "nova":
+            return FULL
+        with self.lock:
+            pend, dec, other = self.n_pending, self.decode_active, self.other
+        if stage == nova.STAGE_DECODE and other is None:
+            return FULL
+        if stage != nova.STAGE_DECODE and dec == 0:
+            return FULL
+        pair = stage if stage != nova.STAGE_DECODE else other
+        op = self.decode_cus[0] if pair == nova.STAGE_ENCODE else self.decode_cus[1]
+        p = sched.decode_cus(pend, op, self.alpha, self.minimum) if self.alpha else op
+        return nova.make_cu_mask(p, 0) if stage == nova.STAGE_DECODE else nova.make_cu_mask(256 - p, p // 8)
+
+    def _stream(self, stage):
+        if self.mode == "time_sliced":
+            return torch.cuda.current_stream()
+        mask = self._masks(stage)
+        s = nova.set_stage_partition(stage, mask)
+        self.partition_log.append((time.perf_counter(), stage, sum(bin(w).count("1") for w in mask)))
+        return s
+
+    # ---------------------------------------------------------------- stage passes
+    def _vision(self, req):
+        s = self._stream(nova.STAGE_ENCODE)
+        req.t_vis0 = time.perf_counter()
+        self.vit.encode(self.pixels, out=self.vis_buf, stream=s)
+        s.synchronize()
+        req.t_vis1 = time.perf_counter()
+
+    def _prefill(self, req):
+        s = self._stream(nova.STAGE_PREFILL)
+        tbl = torch.from_numpy(req.table_row).to("cuda", non_blocking=False)
+        nxt = self.llm.prefill(self.vis_buf[0], req.ids, tbl, self.kv, stream=s)
+        s.synchronize()
+        req.last_token = int(nxt.item())
+        req.t_pre1 = time.perf_counter()
+
+    def _decode_step(self, batch):
+        s = self._stream(nova.STAGE_DECODE)
+        b = len(batch)
+        ids = torch.tensor([r.last_token for r in batch], dtype=torch.int32)
+        pos = torch.tensor([self.n_vis + r.n_text + len(r.t_tokens) for r in batch], dtype=torch.int32)
+        tab = torch.from_numpy(np.stack([r.table_row for r in batch]))
+        max_ctx = int(pos.max()) + 1
+        with torch.cuda.stream(s):
+            ids_d, pos_d, tab_d = ids.cuda(non_blocking=True), pos.cuda(non_blocking=True), tab.cuda(non_blocking=True)
+        nxt = self.llm.decode(ids_d, pos_d, tab_d, self.kv, max_ctx, stream=s)
+        s.synchronize()
+        now = time.perf_counter()
+        out = nxt.cpu()
+        for r, t in zip(batch, out.tolist()):
+            r.last_token = t
+            r.t_tokens.append(now)
+
+    # ---------------------------------------------------------------- admission
+    def _admit(self, req, ids_seed):
+        need = (self.n_vis + req.n_text + req.n_out + self.cfg.block - 1) // self.cfg.block
+        if need > self.max_blocks:
+            raise nova.NovaError(nova.EINVAL, "request longer than the block table")
+        req.blocks = self.blocks.take(need)
+        row = np.full(self.max_blocks, -1, np.int32)
+        row[:need] = req.blocks
+        req.table_row = row
+        req.ids = torch.from_numpy(synth.text_ids(req.n_text, self.cfg.vocab, seed=ids_seed)).to(self.device)
+
+    # ---------------------------------------------------------------- run
+    def run(self, trace, seed=0):
+        for r in trace:
+            self._admit(r, seed * 100003 + r.rid)
+        if self.device == "cuda":
+            torch.cuda.synchronize()
+        if self.mode == "time_sliced":
+            return self._run_sliced(trace)
+        return self._run_threads(trace)
+
+    def _run_threads(self, trace):
+        vq, pq, dq = queue.Queue(), queue.Queue(), queue.Queue()
+        stop = threading.Event()
+
+        def vision_worker():
+            while True:
+                req = vq.get()
+                if req is None:
+                    return
+                self._vision(req)
+                self.events.put(("vision_done", req))
+
+        def prefill_worker():
+            while True:
+                req = pq.get()
+                if req is None:
+                    return
+                self._prefill(req)
+                self.events.put(("prefill_done", req))
+
+        def decode_worker():
+            batch, waiting = [], []
+            while not stop.is_set() or batch or waiting or not dq.empty():
+                try:
+                    while True:
+                        waiting.append(dq.get(block=not batch and not waiting, timeout=0.01))
+                except queue.Empty:
+                    pass
+                while waiting and len(batch) < self.max_batch:     # in-flight batching: join at a step boundary
+                    batch.append(waiting.pop(0))
+                if not batch:
+                    continue
+                self._decode_step(batch)
+                for r in [r for r in batch if r.done]:
+                    batch.remove(r)
+                    self.events.put(("finished", r))
+
+        threads = [threading.Thread(target=f, daemon=True) for f in (vision_worker, prefill_worker, decode_worker)]
+        for t in threads:
+            t.start()
+        t0 = time.perf_counter()
+        pending_arrivals = list(trace)
+        q_vision = []                 # Alg. 1 Q_v: vision requests waiting for encode/prefill to clear
+        busy = {"vision": False, "prefill": False}
+        finished = 0
+
+        def try_vision():
+            if q_vision and not busy["vision"] and not busy["prefill"]:
+                r = q_vision.pop(0)
+                busy["vision"] = True
+                with self.lock:
+                    self.other = nova.STAGE_ENCODE
+                vq.put(r)
+
+        while finished < len(trace):
+            now = time.perf_counter() - t0
+            while pending_arrivals and pending_arrivals[0].arrival <= now:
+                r = pending_arrivals.pop(0)
+                r.t_arrive = t0 + r.arrival
+                with self.lock:
+                    self.n_pending += 1
+                q_vision.append(r)
+                try_vision()
+            timeout = max(0.0, pending_arrivals[0].arrival - now) if pending_arrivals else 0.05
+            try:
+                ev, r = self.events.get(timeout=min(timeout, 0.05))
+            except queue.Empty:
+                continue
+            if ev == "vision_done":
+                busy["vision"] = False
+                busy["prefill"] = True            # prefill goes first, before any further vision
+                with self.lock:
+                    self.other = nova.STAGE_PREFILL
+                pq.put(r)
+            elif ev == "prefill_done":
+                busy["prefill"] = False
+                with self.lock:
+                    self.n_pending -= 1
+                    self.decode_active += 1
+                    self.other = None
+                r.t_tokens.append(r.t_pre1)      # prefill emits the first token
+                if r.done:
+                    self.events.put(("finished", r))
+                else:
+                    dq.put(r)
+                try_vision()
+            elif ev == "finished":
+                with self.lock:
+                    self.decode_active -= 1
+                self.blocks.give(r.blocks)
+                finished += 1
+        stop.set()
+        vq.put(None)
+        pq.put(None)
+        for t in threads:
+            t.join(timeout=30)
+        return summarize(trace)
+
+    def _run_sliced(self, trace):
+        t0 = time.perf_counter()
+        pending = list(trace)
+        q_vision, q_prefill, q_decode, batch = [], [], [], []
+        finished, last_was_decode = 0, False
+        while finished < len(trace):
+            now = time.perf_counter() - t0
+            while pending and pending[0].arrival <= now:
+                r = pending.pop(0)
+                r.t_arrive = t0 + r.arrival
+                q_vision.append(r)
+            while q_decode and len(batch) < self.max_batch:   # join at a step boundary
+                batch.append(q_decode.pop(0))
+            if batch and (not last_was_decode or (not q_prefill and not q_vision)):
+                self._decode_step(batch)
+                last_was_decode = True
+                for r in [r for r in batch if r.done]:
+                    batch.remove(r)
+                    self.blocks.give(r.blocks)
+                    finished += 1
+                continue
+            last_was_decode = False
+            if q_prefill:
+                r = q_prefill.pop(0)
+                self._prefill(r)
+                r.t_tokens.append(r.t_pre1)
+                if r.done:
+                    self.blocks.give(r.blocks)
+                    finished += 1
+                else:
+                    q_decode.append(r)
+                continue
+            if q_vision:
+                r = q_vision.pop(0)
+                self._vision(r)
+                q_prefill.append(r)
+                continue
+            if pending:
+                time.sleep(max(0.0, min(0.002, pending[0].arrival - (time.perf_counter() - t0))))
+        return summarize(trace)
+
+
+def summarize(trace):
+    e2e = np.array([r.t_tokens[-1] - r.t_arrive for r in trace])
+    ttft = np.array([r.t_pre1 - r.t_arrive for r in trace])
+    tbt = np.array([np.mean(np.diff(r.t_tokens)) if len(r.t_tokens) > 1 else 0.0 for r in trace])
+    qwait = np.array([r.t_vis0 - r.t_arrive for r in trace])
+    span = max(r.t_tokens[-1] for r in trace) - min(r.t_arrive for r in trace)
+    return {"requests": len(trace), "max_e2e_s": round(float(e2e.max()), 4), "avg_e2e_s": round(float(e2e.mean()), 4),
+            "p50_e2e_s": round(float(np.median(e2e)), 4), "avg_ttft_s": round(float(ttft.mean()), 4),
+            "avg_tbt_ms": round(float(tbt.mean()) * 1e3, 3), "max_tbt_ms": round(float(tbt.max()) * 1e3, 3),
+            "avg_queue_wait_s": round(float(qwait.mean()), 4), "throughput_req_s": round(len(trace) / span, 3)}

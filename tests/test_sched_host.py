@@ -1,0 +1,58 @@
+"""Host-side partition planning (paper_2509_21301_amd.sched) against the oracle's statement of
+Eq. 1-5 on the same curves (the two are written independently)."""
+import numpy as np
+
+from oracle import sched as osched
+from paper_2509_21301_amd import sched
+
+SHARES = [32, 64, 96, 128, 160, 192, 224]
+
+
+def curves(seed):
+    r = np.random.default_rng(seed)
+    tv = {p: 0.03 * 256 / (256 - p) * (1 + 0.1 * r.random()) for p in SHARES}
+    tp = {p: 0.02 * 256 / (256 - p) * (1 + 0.1 * r.random()) for p in SHARES}
+    dv = {p: 0.004 * 256 / p * (1 + 0.2 * r.random()) for p in SHARES}
+    dp = {p: 0.005 * 256 / p * (1 + 0.2 * r.random()) for p in SHARES}
+    return sched.StageCurves(SHARES, tv, tp, dv, dp)
+
+
+def test_e2e_and_best_static_match_oracle():
+    for seed in range(5):
+        c = curves(seed)
+        for out_len in (16, 32, 48):
+            for pv in SHARES:
+                for pp in SHARES:
+                    ref = osched.e2e_latency(c.t_vision[pv], c.t_prefill[pp], c.t_dec_vision[pv], c.t_dec_prefill[pp], out_len)
+                    assert abs(sched.expected_e2e(c, pv, pp, out_len) - ref) < 1e-12
+            pv, pp, lat = sched.best_static(c, out_len)
+            opv, opp, olat = osched.optimal_partition(SHARES, c.t_vision, c.t_prefill, c.t_dec_vision,
+                                                      c.t_dec_prefill, out_len)
+            assert (pv, pp) == (opv, opp) and abs(lat - olat) < 1e-12
+
+
+def test_pareto_front_matches_oracle():
+    c = curves(11)
+    front = sched.pareto_front(c, 32)
+    pts = [(sched.expected_e2e(c, a, b, 32), sched.ideal_throughput(c, a, b), (a, b)) for a in SHARES for b in SHARES]
+    ref = osched.pareto_front(pts)
+    assert [(f[2], f[3]) for f in front] == [p[2] for p in ref]
+    lats = [f[0] for f in front]
+    thrs = [f[1] for f in front]
+    assert lats == sorted(lats) and thrs == sorted(thrs)
+    assert abs(front[0][1] - osched.throughput(c.t_vision[front[0][2]], c.t_prefill[front[0][3]])) < 1e-12
+
+
+def test_decode_share_eq5():
+    for n in range(1, 8):
+        assert sched.decode_cus(n, 96, 16, 32) == osched.decode_share(96, 16, 32, n)
+    assert sched.decode_cus(0, 96, 16, 32) == 96
+    assert sched.decode_cus(2, 100, 4, 12) == 96           # rounded down to the 8-CU granule
+    assert sched.decode_cus(9, 100, 40, 4) == 8
+
+
+def test_from_corun_records():
+    recs = [{"pair": "decode+encode", "decode_cus": 64, "encode_ms_corun": 50.0, "decode_step_ms_corun": 12.0},
+            {"pair": "decode+prefill", "decode_cus": 64, "prefill_ms_corun": 56.0, "decode_step_ms_corun": 12.5}]
+    c = sched.StageCurves.from_corun(recs)
+    assert c.shares == [64] and c.t_vision[64] == 0.05 and c.t_dec_prefill[64] == 0.0125
