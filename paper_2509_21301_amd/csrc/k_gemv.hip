@@ -1,15 +1,19 @@
 // Thin GEMM for the decode linears and the LM head: Y[B,N] = X[B,K] W[N,K]^T, B <= 32.
 //
 // Decode is bound by streaming the weights from HBM (the paper's Table 3 decode row and
-// Sec. 3.2.1).  Each wave streams 32 weight rows with 16-byte loads (16 per lane per 256-wide
-// K chunk, 32 in flight with the prefetch), and feeds them to MFMA 16x16x32 as
-// the A operand with the batch as the 16-wide B operand (a second MFMA covers rows 16..31 of
-// the batch).  X fragments come straight from L2 (X is small and shared by every workgroup);
-// weight loads run one chunk ahead of the MFMAs, with no LDS and no barriers.  When N alone
-// gives too few workgroups, K is split and a small second pass reduces the fp32 partials and applies the
-// epilogue; otherwise the epilogue is applied directly.
-// The k index of an MFMA fragment only has to agree between its A and B operands, which leaves
-// the assignment of k pieces to lanes free; it is chosen for coalescing.
+// Sec. 3.2.1).  Each wave owns 16 weight rows and walks K in 256-wide chunks.  A chunk is read
+// with eight 16-byte-per-lane loads, each covering two whole rows (2 x 512 contiguous bytes):
+// loads that touch only part of a cache line per row cost far more per byte on a CU, which shows
+// most when the stream runs on a fraction of the chip.  The chunk then passes through a
+// wave-private LDS tile into the MFMA 16x16x32 operand layout (row = lane % 16), with an XOR
+// swizzle that keeps both the writes and the reads free of bank conflicts.  The batch is the
+// other MFMA operand: X chunks stream through a two-slot LDS ring shared by the workgroup's four
+// waves, one barrier per chunk.  Weight and X loads run two chunks ahead in registers, issued in
+// the order they are consumed so that each wait covers only its own chunk.
+// When N alone gives too few workgroups, K is split and a small second pass reduces the fp32
+// partials and applies the epilogue; otherwise the epilogue is applied directly.
+// The k index of an MFMA fragment only has to agree between its two operands, which leaves the
+// assignment of k pieces to lanes free.
 #include <algorithm>
 
 #include "common.hpp"
@@ -17,117 +21,174 @@
 
 namespace nova {
 
-constexpr int GV_KC = 256;          // K chunk per pipeline step
-
-constexpr int GV_RW = 16;           // weight rows per wave
+constexpr int GV_KC = 256;             // K chunk per pipeline step (32 pieces of 8)
+constexpr int GV_RW = 16;              // weight rows per wave
+constexpr int GV_ROWS = 4 * GV_RW;     // rows per workgroup (4 waves)
 constexpr int GV_MAX_SPLITS = 16;
 
-// K splits so that the launch has about 2048 waves (every CU holding several); a split is a
-// run of whole 256-wide chunks, the last one possibly shorter.
-int gemv_splits(int N, int K) {
+// K splits: enough waves to occupy every CU (about 2048 16-row waves), and each split a run of
+// whole 256-wide chunks with no empty split.
+int gemv_splits(int N, int K, int B, bool f32x) {
+  (void)B;
+  (void)f32x;
   const int chunks = K / GV_KC, waves = N / GV_RW;
-  if (waves >= 2048) return 1;
-  int s = std::min((2048 + waves - 1) / waves, GV_MAX_SPLITS);
+  int s = waves >= 2048 ? 1 : std::min((2048 + waves - 1) / waves, GV_MAX_SPLITS);
   s = std::min(s, chunks);
   const int per = (chunks + s - 1) / s;          // chunks per split
-  return (chunks + per - 1) / per;               // no empty split
+  return (chunks + per - 1) / per;
 }
 
-size_t gemv_partial_floats(int B, int N, int K) {
-  const int s = gemv_splits(N, K);
+size_t gemv_partial_floats(int B, int N, int K, bool f32x) {
+  const int s = gemv_splits(N, K, B, f32x);
   return s > 1 ? (size_t)s * B * N : 0;
 }
 
-template <typename TX, typename OT, int NB, int EPI, bool DIRECT, int RW>
+// Element (row, k) of a 256-wide tile with rows of 32 16-byte pieces: piece k/8 is stored at
+// slot (k/8) ^ (row % 16).
+__device__ __forceinline__ int swz(int row, int piece) { return row * GV_KC + 8 * (piece ^ (row & 15)); }
+
+template <typename TX, typename OT, int NB, int EPI, bool DIRECT>
 __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
   constexpr bool F32X = sizeof(TX) == 4;
-  constexpr int RG = RW / 16;                  // 16-row MFMA groups per wave
-  constexpr int XN = F32X ? 2 : 1;             // 16-byte pieces per X fragment
+  constexpr int XROWS = 16 * NB;                          // batch rows held (B padded)
+  constexpr int XR = F32X ? 1 : 2;                        // X ring slots
+  constexpr int XSLOT = XROWS * GV_KC * (F32X ? 2 : 1);   // bf16 per slot (fp32 mode: hi, lo)
+  constexpr int XPT = XROWS / 8;                          // 16-byte X pieces per thread per chunk
+  constexpr int XL = F32X ? 2 * XPT : XPT;                // X loads per thread per chunk
+  __shared__ __align__(16) bf16_t wt[4][GV_RW * GV_KC];
+  __shared__ __align__(16) bf16_t xs[XR * XSLOT];
+
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n_base = blockIdx.x * (4 * RW) + wave * RW;
+  const int n_base = blockIdx.x * GV_ROWS + wave * GV_RW;
   const int split = blockIdx.y;
   const int k_begin = split * kc, k_end = min(k_begin + kc, p.K);
-  const int row = lane & 15, g = lane >> 4;
-  // Fragment u of a 256-wide chunk holds k = k0 + 8 * (4u + g) .. +8: the four lanes of a row
-  // read 64 adjacent bytes per instruction and two instructions complete each 128-byte line.
-  const bf16_t* wrow = p.W + (size_t)(n_base + row) * p.ldw + 8 * g;
+  const int nchunks = (k_end - k_begin) / GV_KC;
+  const int n = lane & 15, g = lane >> 4;          // MFMA operand row and k group
+  const int h = lane >> 5, pc = lane & 31;         // load row within a pair, piece
+
+  // weight load i of a chunk: rows 2i + h, piece pc (lanes 0-31 and 32-63 each read one row)
+  const bf16_t* wsrc = p.W + (size_t)(n_base + h) * p.ldw + k_begin + 8 * pc;
+  typedef u32x4 WBuf[8];
+  auto load_w = [&](int c, WBuf& w) {
+    const bf16_t* src = wsrc + (size_t)min(c, nchunks - 1) * GV_KC;   // tail: re-read the last chunk
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = *reinterpret_cast<const u32x4*>(src + (size_t)(2 * i) * p.ldw);
+  };
+  // X piece q of a chunk for this thread: batch row tid / 32 + 8q (clamped to B-1: those rows
+  // only feed output columns that are never stored), piece tid % 32
   const TX* X = reinterpret_cast<const TX*>(p.X);
-
-  f32x4 acc[RG][NB];
+  typedef u32x4 XBuf[XL];
+  auto load_x = [&](int c, XBuf& x) {
+    const int k = k_begin + min(c, nchunks - 1) * GV_KC + 8 * pc;
 #pragma unroll
-  for (int i = 0; i < RG; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  typedef u32x4 WBuf[RG][8];
-  typedef u32x4 XBuf[NB][8][XN];
-  auto load = [&](int k0, WBuf& w, XBuf& x) {
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-#pragma unroll
-      for (int i = 0; i < RG; ++i) w[i][u] = *reinterpret_cast<const u32x4*>(wrow + (size_t)16 * i * p.ldw + k0 + 32 * u);
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int b = j * 16 + row;
-      const u32x4* xr = reinterpret_cast<const u32x4*>(X + (size_t)b * p.ldx + k0 + 8 * g);
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int h = 0; h < XN; ++h) x[j][u][h] = b < p.B ? xr[(32 * u) / (8 / XN) + h] : u32x4{0u, 0u, 0u, 0u};
+    for (int q = 0; q < XPT; ++q) {
+      const TX* src = X + (size_t)min((tid >> 5) + 8 * q, p.B - 1) * p.ldx + k;
+      if constexpr (F32X) {
+        x[2 * q] = *reinterpret_cast<const u32x4*>(src);
+        x[2 * q + 1] = *reinterpret_cast<const u32x4*>(src + 4);
+      } else {
+        x[q] = *reinterpret_cast<const u32x4*>(src);
+      }
     }
   };
-  auto compute = [&](const WBuf& w, const XBuf& x) {
+  auto store_x = [&](const XBuf& x, int slot) {
+    bf16_t* dst = xs + slot * XSLOT;
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        Frag8 fx, fl;
-        if constexpr (F32X) {
-          float x8[8];
-          *reinterpret_cast<u32x4*>(x8) = x[j][u][0];
-          *reinterpret_cast<u32x4*>(x8 + 4) = x[j][u][XN - 1];
-          split8(x8, fx, fl);
-        } else {
-          fx = __builtin_bit_cast(Frag8, x[j][u][0]);
-        }
-#pragma unroll
-        for (int i = 0; i < RG; ++i) {
-          acc[i][j] = mfma16(__builtin_bit_cast(Frag8, w[i][u]), fx, acc[i][j]);
-          if constexpr (F32X) acc[i][j] = mfma16(__builtin_bit_cast(Frag8, w[i][u]), fl, acc[i][j]);
-        }
+    for (int q = 0; q < XPT; ++q) {
+      const int r = (tid >> 5) + 8 * q;
+      if constexpr (F32X) {
+        float x8[8];
+        *reinterpret_cast<u32x4*>(x8) = x[2 * q];
+        *reinterpret_cast<u32x4*>(x8 + 4) = x[2 * q + 1];
+        Frag8 hi, lo;
+        split8(x8, hi, lo);
+        *reinterpret_cast<Frag8*>(dst + swz(r, pc)) = hi;
+        *reinterpret_cast<Frag8*>(dst + XROWS * GV_KC + swz(r, pc)) = lo;
+      } else {
+        *reinterpret_cast<u32x4*>(dst + swz(r, pc)) = x[q];
       }
+    }
   };
 
-  // double buffer: chunk c+1's weights and activations are in flight while chunk c computes
-  WBuf w0, w1;
-  XBuf x0, x1;
-  load(k_begin, w0, x0);
-  for (int k0 = k_begin; k0 < k_end; k0 += 2 * GV_KC) {
-    const bool has1 = k0 + GV_KC < k_end;
-    if (has1) load(k0 + GV_KC, w1, x1);
-    compute(w0, x0);
-    if (!has1) break;
-    if (k0 + 2 * GV_KC < k_end) load(k0 + 2 * GV_KC, w0, x0);
-    compute(w1, x1);
+  f32x4 acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16_t* tw = wt[wave];
+
+  // one chunk: weights through the wave's tile into operand layout, then MFMAs against the X slot;
+  // MFMA u takes piece 4u + g of row n from both operands
+  auto compute = [&](int c, const WBuf& w) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(tw + swz(2 * i + h, pc)) = w[i];
+    // a wave's LDS operations execute in order; only the compiler has to be kept from moving
+    // the reads above the writes (or the next chunk's writes above these reads)
+    asm volatile("" ::: "memory");
+    const bf16_t* xb = xs + (c % XR) * XSLOT;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const Frag8 wf = *reinterpret_cast<const Frag8*>(tw + swz(n, 4 * u + g));
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const Frag8 xf = *reinterpret_cast<const Frag8*>(xb + swz(16 * j + n, 4 * u + g));
+        acc[j] = mfma16(wf, xf, acc[j]);
+        if constexpr (F32X) {
+          const Frag8 xl = *reinterpret_cast<const Frag8*>(xb + XROWS * GV_KC + swz(16 * j + n, 4 * u + g));
+          acc[j] = mfma16(wf, xl, acc[j]);
+        }
+      }
+    }
+    asm volatile("" ::: "memory");
+  };
+  // compute chunk c, then publish X(c+1) in its ring slot (with one slot, only after every wave
+  // is done with chunk c); the barrier makes it visible and frees the other slot
+  auto step = [&](int c, const WBuf& w, const XBuf& xnext) {
+    compute(c, w);
+    if (c + 1 < nchunks) {
+      if constexpr (XR == 1) __syncthreads();
+      store_x(xnext, (c + 1) % XR);
+    }
+    __syncthreads();
+  };
+
+  // loads are unconditional (clamped at the tail) and issued in consumption order, so that the
+  // wait before each use covers only its own chunk
+  WBuf w0, w1, w2;
+  XBuf x0, x1, x2;
+  load_x(0, x0);
+  load_w(0, w0);
+  load_x(1, x1);
+  load_w(1, w1);
+  store_x(x0, 0);
+  __syncthreads();
+  for (int c = 0; c < nchunks; c += 3) {
+    load_x(c + 2, x2);
+    load_w(c + 2, w2);
+    step(c, w0, x1);
+    load_x(c + 3, x0);
+    load_w(c + 3, w0);
+    if (c + 1 < nchunks) step(c + 1, w1, x2);
+    load_x(c + 4, x1);
+    load_w(c + 4, w1);
+    if (c + 2 < nchunks) step(c + 2, w2, x0);
   }
 
   // lane holds D[n = 4*(lane/16) + r][b = lane%16] of each 16x16 tile
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int b = j * 16 + (lane & 15);
-    if constexpr (EPI == EPI_ARGMAX) {
+    if constexpr (EPI == EPI_ARGMAX && DIRECT) {
       // greedy argmax fused into the LM head: best (logit, lowest id) of the lane's 4 rows, then
       // of the 16 rows of the tile (lanes 16 apart), merged across workgroups by a 64-bit
       // atomic max on (order-preserving logit bits, ~id)
       unsigned long long key = 0ull;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int n = n_base + (lane >> 4) * 4 + r;
-        const float v = acc[0][j][r];
-        if (DIRECT && p.out != nullptr && b < p.B) reinterpret_cast<float*>(p.out)[(size_t)b * p.ldo + n] = v;
+        const int nr = n_base + (lane >> 4) * 4 + r;
+        const float v = acc[j][r];
+        if (p.out != nullptr && b < p.B) reinterpret_cast<float*>(p.out)[(size_t)b * p.ldo + nr] = v;
         const uint32_t u = __float_as_uint(v);
         const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-        const unsigned long long k = ((unsigned long long)ord << 32) | (uint32_t)~(uint32_t)n;
+        const unsigned long long k = ((unsigned long long)ord << 32) | (uint32_t)~(uint32_t)nr;
         key = k > key ? k : key;
       }
 #pragma unroll
@@ -138,35 +199,23 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
       if (lane < 16 && b < p.B) atomicMax(p.argmax_keys + b, key);
       continue;
     }
-    if constexpr (EPI == EPI_SWIGLU) {
-      if (j * 16 >= p.B) continue;    // whole column group empty (uniform across the wave)
-    } else {
-      if (b >= p.B) continue;
-    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int nr = (lane >> 4) * 4 + r;
       if constexpr (!DIRECT) {
-        float* part = p.partial + ((size_t)split * p.B + b) * p.N;
-#pragma unroll
-        for (int i = 0; i < RG; ++i) part[n_base + 16 * i + nr] = acc[i][j][r];
+        if (b < p.B) p.partial[((size_t)split * p.B + b) * p.N + n_base + nr] = acc[j][r];
       } else if constexpr (EPI == EPI_SWIGLU) {
-        if (b >= p.B) continue;
         // rows interleaved in blocks of 8: rows 0-7 of the tile are gate rows, 8-15 the matching
         // up rows, held by lanes 32 apart
-        const float gte = acc[0][j][r], up = __shfl_xor(acc[0][j][r], 32, 64);
-        if (lane < 32) {
+        const float up = __shfl_xor(acc[j][r], 32, 64);
+        if (lane < 32 && b < p.B) {
           const int oc = (n_base >> 1) + nr;
-          reinterpret_cast<OT*>(p.out)[(size_t)b * p.ldo + oc] = from_f<OT>(silu(gte) * up);
+          reinterpret_cast<OT*>(p.out)[(size_t)b * p.ldo + oc] = from_f<OT>(silu(acc[j][r]) * up);
         }
       } else if constexpr (EPI == EPI_RESID) {
-        float* o = reinterpret_cast<float*>(p.out) + (size_t)b * p.ldo;
-#pragma unroll
-        for (int i = 0; i < RG; ++i) o[n_base + 16 * i + nr] += acc[i][j][r];
+        if (b < p.B) reinterpret_cast<float*>(p.out)[(size_t)b * p.ldo + n_base + nr] += acc[j][r];
       } else {
-        OT* o = reinterpret_cast<OT*>(p.out) + (size_t)b * p.ldo;
-#pragma unroll
-        for (int i = 0; i < RG; ++i) o[n_base + 16 * i + nr] = from_f<OT>(acc[i][j][r]);
+        if (b < p.B) reinterpret_cast<OT*>(p.out)[(size_t)b * p.ldo + n_base + nr] = from_f<OT>(acc[j][r]);
       }
     }
   }
@@ -177,14 +226,30 @@ template <typename OT, int EPI>
 __global__ void gemv_reduce(GemvArgs p, int splits) {
   const int ncols = EPI == EPI_SWIGLU ? p.N / 2 : p.N;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long)p.B * ncols) return;
-  const int b = (int)(idx / ncols), c = (int)(idx % ncols);
+  const bool live = idx < (long)p.B * ncols;
+  const int b = live ? (int)(idx / ncols) : 0, c = live ? (int)(idx % ncols) : 0;
   auto sum = [&](int n) {
     float v = 0.f;
 #pragma unroll 4
     for (int s = 0; s < splits; ++s) v += p.partial[((size_t)s * p.B + b) * p.N + n];
     return v;
   };
+  if constexpr (EPI == EPI_ARGMAX) {
+    // logits of one row are contiguous and ncols is a multiple of 64, so a wave shares one b
+    const float v = live ? sum(c) : -INFINITY;
+    if (live && p.out != nullptr) reinterpret_cast<float*>(p.out)[(size_t)b * p.ldo + c] = v;
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    unsigned long long key = live ? (((unsigned long long)ord << 32) | (uint32_t)~(uint32_t)c) : 0ull;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const unsigned long long other = __shfl_xor(key, o, 64);
+      key = other > key ? other : key;
+    }
+    if ((threadIdx.x & 63) == 0 && key != 0ull) atomicMax(p.argmax_keys + b, key);
+    return;
+  }
+  if (!live) return;
   if constexpr (EPI == EPI_SWIGLU) {
     const int n = (c >> 3) * 16 + (c & 7);     // gate row; its up row is 8 further
     reinterpret_cast<OT*>(p.out)[(size_t)b * p.ldo + c] = from_f<OT>(silu(sum(n)) * sum(n + 8));
@@ -197,18 +262,20 @@ __global__ void gemv_reduce(GemvArgs p, int splits) {
 
 template <typename TX, typename OT, int NB, int EPI>
 static hipError_t gemv_launch(const GemvArgs& p, hipStream_t s) {
-  const int splits = EPI == EPI_ARGMAX ? 1 : gemv_splits(p.N, p.K);   // the fused argmax needs whole rows
+  constexpr bool F32X = sizeof(TX) == 4;
+  const int splits = gemv_splits(p.N, p.K, p.B, F32X);
   const int chunks = p.K / GV_KC;
   const int kc = (chunks + splits - 1) / splits * GV_KC;
-  dim3 grid(p.N / (4 * GV_RW), splits);
+  dim3 grid(p.N / GV_ROWS, splits);
   if (splits == 1) {
-    hipLaunchKernelGGL((gemv_kernel<TX, OT, NB, EPI, true, GV_RW>), grid, dim3(256), 0, s, p, kc);
+    hipLaunchKernelGGL((gemv_kernel<TX, OT, NB, EPI, true>), grid, dim3(256), 0, s, p, kc);
     return hipGetLastError();
   }
-  if (EPI == EPI_ARGMAX || !p.partial) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((gemv_kernel<TX, OT, NB, EPI, false, GV_RW>), grid, dim3(256), 0, s, p, kc);
+  if (!p.partial) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((gemv_kernel<TX, OT, NB, EPI, false>), grid, dim3(256), 0, s, p, kc);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.out == nullptr) return e;      // out == null: the caller reduces the partials
+  // out == null (except for the argmax, whose logits are optional): the caller reduces the partials
+  if (e != hipSuccess || (p.out == nullptr && EPI != EPI_ARGMAX)) return e;
   const long n = (long)p.B * (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
   hipLaunchKernelGGL((gemv_reduce<OT, EPI>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, splits);
   return hipGetLastError();
@@ -217,8 +284,8 @@ static hipError_t gemv_launch(const GemvArgs& p, hipStream_t s) {
 template <typename TX, typename OT>
 hipError_t gemv(const GemvArgs& p, int epi, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  if (p.B > 32 || p.N % 64 || p.K % GV_KC || p.ldx % 8 || p.ldw % 8) return hipErrorInvalidValue;
-  if (epi == EPI_ARGMAX && !p.argmax_keys) return hipErrorInvalidValue;
+  if (p.B > 32 || p.N % GV_ROWS || p.K <= 0 || p.K % GV_KC || p.ldx % 8 || p.ldw % 8) return hipErrorInvalidValue;
+  if (epi == EPI_ARGMAX && (!p.argmax_keys || p.N % 64)) return hipErrorInvalidValue;
   const bool two = p.B > 16;
 #define NOVA_GEMV_CASE(E)                                                             \
   case E: return two ? gemv_launch<TX, OT, 2, E>(p, s) : gemv_launch<TX, OT, 1, E>(p, s);

@@ -41,8 +41,8 @@ struct GemvArgs {
   float* partial;
   unsigned long long* argmax_keys;
 };
-int gemv_splits(int N, int K);
-size_t gemv_partial_floats(int B, int N, int K);
+int gemv_splits(int N, int K, int B, bool f32x);
+size_t gemv_partial_floats(int B, int N, int K, bool f32x);
 template <typename TX, typename OT>
 hipError_t gemv(const GemvArgs& p, int epi, hipStream_t s);
 

@@ -532,11 +532,12 @@ size_t decode_ws(const nova_llm* m, int B, int max_ctx, Carve* cv) {
   w.take<unsigned long long>((size_t)B);                // argmax keys
   size_t part = 0;
   const int qd = c.n_q * c.head_dim;
-  part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden));
-  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, qd));
-  part = std::max(part, nova::gemv_partial_floats(B, 2 * m->ip, c.hidden));
-  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, m->ip));
-  part = std::max(part, nova::gemv_partial_floats(B, c.vocab, c.hidden));
+  const bool f32 = sizeof(T) == 4;
+  part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden, f32));
+  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, qd, f32));
+  part = std::max(part, nova::gemv_partial_floats(B, 2 * m->ip, c.hidden, f32));
+  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, m->ip, f32));
+  part = std::max(part, nova::gemv_partial_floats(B, c.vocab, c.hidden, f32));
   w.take<float>(part);
   w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, c.head_dim, max_ctx, c.n_kv));
   return w.used;
@@ -624,21 +625,22 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
   T* att = w.take<T>((size_t)B * qd);
   T* hm = w.take<T>((size_t)B * m->ip);
   unsigned long long* keys = w.take<unsigned long long>((size_t)B);
+  const bool f32 = sizeof(T) == 4;
   size_t partn = 0;
-  partn = std::max(partn, nova::gemv_partial_floats(B, m->qkvw, H));
-  partn = std::max(partn, nova::gemv_partial_floats(B, H, qd));
-  partn = std::max(partn, nova::gemv_partial_floats(B, 2 * m->ip, H));
-  partn = std::max(partn, nova::gemv_partial_floats(B, H, m->ip));
-  partn = std::max(partn, nova::gemv_partial_floats(B, c.vocab, H));
+  partn = std::max(partn, nova::gemv_partial_floats(B, m->qkvw, H, f32));
+  partn = std::max(partn, nova::gemv_partial_floats(B, H, qd, f32));
+  partn = std::max(partn, nova::gemv_partial_floats(B, 2 * m->ip, H, f32));
+  partn = std::max(partn, nova::gemv_partial_floats(B, H, m->ip, f32));
+  partn = std::max(partn, nova::gemv_partial_floats(B, c.vocab, H, f32));
   float* part = w.take<float>(partn);
   float* apart = w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, D, max_ctx, c.n_kv));
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
 
   // Split-K projections leave their partials for the next kernel: the QKV partials are summed by
   // the rotary/KV-append kernel, the O and down partials by the fused residual + RMSNorm.
-  const int sp_qkv = nova::gemv_splits(m->qkvw, H);
-  const int sp_o = nova::gemv_splits(H, qd);
-  const int sp_down = nova::gemv_splits(H, m->ip);
+  const int sp_qkv = nova::gemv_splits(m->qkvw, H, B, f32);
+  const int sp_o = nova::gemv_splits(H, qd, B, f32);
+  const int sp_down = nova::gemv_splits(H, m->ip, B, f32);
   const char* hw = (const char*)m->d.head;
   auto layer_w = [&](int l, int i) {
     return (const bf16_t*)((const char*)m->d.layers + (size_t)l * m->lay.bytes + m->lay.off[i]);
@@ -682,7 +684,7 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
                                                    next_gain, c.eps, a, H, l + 1 < c.layers ? nullptr : keys, s));
   }
   {
-    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, nullptr, keys};
+    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, part, keys};
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
   CALL(NOVA_KIND_MISC, s, nova::argmax_finish(keys, B, next_ids, s));
