@@ -2,14 +2,17 @@
 //
 // These are the QKV, output-projection, MLP up/gate and down linears that dominate vision encode
 // and prefill time (the paper's Table 3 and Sec. 3.2.1).  Design for gfx950:
-//  * bf16 MFMA 16x16x32 (fp32 accumulate); four waves per workgroup, each owning a WM x WN tile;
-//  * A and W tiles staged through LDS with a 16-byte row pad (conflict-free ds_read_b128),
-//    double-buffered so the global loads of tile k+1 overlap the MFMAs of tile k;
+//  * bf16 MFMA 16x16x32 (fp32 accumulate); 4 or 8 waves per workgroup, each owning a WM x WN tile;
+//  * bf16 activations: A and W tiles go global -> LDS by 16-byte LDS-DMA loads in an XOR-swizzled
+//    layout (conflict-free fragment reads), two stages, the DMA of step k+1 in flight during the
+//    MFMAs of step k;
+//  * fp32 activations (tiny-stack exact mode): tiles staged through registers (split into bf16
+//    hi + lo parts, two MFMAs each, since weights are exactly bf16) into a padded LDS layout;
 //  * tile order remapped so that each XCD (which owns one L2) works on a contiguous block of
 //    output tiles: the dispatcher deals workgroups to the 8 XCDs round-robin;
-//  * fp32 activations (tiny-stack exact mode) are split into bf16 hi + lo parts, two MFMAs each,
-//    since weights are exactly bf16.
-// Requirements (checked by the host): N % BN == 0, K % 64 == 0, 16-byte aligned rows.
+//  * the epilogue (bias, GELU, SwiGLU, residual or position add) runs through LDS so that every
+//    global access covers whole cache lines.
+// Requirements (checked by the host): N % 128 == 0, K % 64 == 0, 16-byte aligned rows, ldo % 4 == 0.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -18,6 +21,99 @@ namespace nova {
 constexpr int BK = 64;
 constexpr int PAD = 8;             // bf16 elements of row padding in LDS
 constexpr int LDK = BK + PAD;      // LDS row pitch (elements)
+
+// Four consecutive outputs: one 16-byte (fp32) or 8-byte (bf16) store.
+template <typename OT>
+__device__ __forceinline__ void store4(OT* dst, const float v[4]) {
+  if constexpr (sizeof(OT) == 4) {
+    *reinterpret_cast<float4*>(dst) = float4{v[0], v[1], v[2], v[3]};
+  } else {
+    *reinterpret_cast<uint2*>(dst) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+  }
+}
+
+// Epilogue, through LDS (free after the main loop's last barrier): each wave stages one 16-row
+// block of its WM x WN tile at a time in a private fp32 scratch, then reads it back along rows so
+// that every global access covers whole cache lines (the MFMA layout gives a lane one column
+// of 4 rows).  row0/col0: the wave tile's first output row and column.
+template <typename OT, int EPI, int WM, int WN>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x4 (&acc)[WM / 16][WN / 16], float* smem,
+                                              int wave, int lane, int row0, int col0) {
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int SP = WN + 4;                         // scratch pitch: the writes of rows 4 apart
+  constexpr bool SW = EPI == EPI_SWIGLU;
+  constexpr int LPR = SW ? WN / 8 : WN / 4;          // lanes per scratch row
+  constexpr int RPI = 64 / LPR, NP = 16 / RPI;       // rows per pass, passes per block
+  float* sc = smem + wave * 16 * SP;                 // land 16 banks apart
+  const int er = (lane >> 4) * 4, ec = lane & 15;
+  const int q = lane % LPR, prow = lane / LPR;
+  // this lane's columns are the same in every pass: 4 consecutive ones, or for SwiGLU (W rows
+  // interleaved in blocks of 8: of each 16 columns, 0-7 gate and 8-15 the matching up rows)
+  // 4 gate columns and the 4 up columns 8 further, giving 4 outputs
+  const int c = SW ? (q >> 1) * 16 + (q & 1) * 4 : q * 4;
+  const int n = col0 + c;
+  const int nout = SW ? (col0 >> 1) + (q >> 1) * 8 + (q & 1) * 4 : n;
+  float bias[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (!SW) {
+    if (p.bias) {
+      const uint2 bb = *reinterpret_cast<const uint2*>(p.bias + n);
+      bias[0] = bf2f((bf16_t)(bb.x & 0xffff)); bias[1] = bf2f((bf16_t)(bb.x >> 16));
+      bias[2] = bf2f((bf16_t)(bb.y & 0xffff)); bias[3] = bf2f((bf16_t)(bb.y >> 16));
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sc[(er + r) * SP + j * 16 + ec] = acc[i][j][r];
+    // a wave's LDS operations execute in order; keep the compiler from reordering them
+    asm volatile("" ::: "memory");
+    float4 v[NP], u[NP];
+#pragma unroll
+    for (int t = 0; t < NP; ++t) {
+      const int row = t * RPI + prow;
+      v[t] = *reinterpret_cast<const float4*>(sc + row * SP + c);
+      if constexpr (SW) u[t] = *reinterpret_cast<const float4*>(sc + row * SP + c + 8);
+    }
+    asm volatile("" ::: "memory");
+    // residual / position rows are read for every pass first (rows past M clamped), then stored
+    float4 x[NP];
+    if constexpr (EPI == EPI_RESID || EPI == EPI_POS) {
+#pragma unroll
+      for (int t = 0; t < NP; ++t) {
+        const int m = min(row0 + i * 16 + t * RPI + prow, p.M - 1);
+        if constexpr (EPI == EPI_RESID) {
+          x[t] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.out) + (size_t)m * p.ldo + n);
+        } else {
+          const uint2 pp = *reinterpret_cast<const uint2*>(p.pos + (size_t)(m % p.pos_rows) * p.N + n);
+          x[t] = float4{bf2f((bf16_t)(pp.x & 0xffff)), bf2f((bf16_t)(pp.x >> 16)),
+                        bf2f((bf16_t)(pp.y & 0xffff)), bf2f((bf16_t)(pp.y >> 16))};
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NP; ++t) {
+      const int m = row0 + i * 16 + t * RPI + prow;
+      if (m >= p.M) continue;
+      float o[4] = {v[t].x + bias[0], v[t].y + bias[1], v[t].z + bias[2], v[t].w + bias[3]};
+      if constexpr (SW) {
+        o[0] = silu(v[t].x) * u[t].x; o[1] = silu(v[t].y) * u[t].y;
+        o[2] = silu(v[t].z) * u[t].z; o[3] = silu(v[t].w) * u[t].w;
+        store4<OT>(reinterpret_cast<OT*>(p.out) + (size_t)m * p.ldo + nout, o);
+      } else if constexpr (EPI == EPI_STORE) {
+        store4<OT>(reinterpret_cast<OT*>(p.out) + (size_t)m * p.ldo + n, o);
+      } else if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = gelu_erf(o[e]);
+        store4<OT>(reinterpret_cast<OT*>(p.out) + (size_t)m * p.ldo + n, o);
+      } else {   // RESID, POS: fp32 out
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.out) + (size_t)m * p.ldo + n) =
+            float4{o[0] + x[t].x, o[1] + x[t].y, o[2] + x[t].z, o[3] + x[t].w};
+      }
+    }
+  }
+}
 
 template <typename TA, typename OT, int EPI, int BM, int BN, int WM, int WN>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_kernel(GemmArgs p) {
@@ -143,53 +239,149 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_kernel(GemmAr
     __syncthreads();
   }
 
-  // ---- epilogue: lane holds rows 4*(lane/16)+r, column lane%16 of each 16x16 tile
-  const int er = (lane >> 4) * 4, ec = lane & 15;
+  gemm_epilogue<OT, EPI, WM, WN>(p, acc, reinterpret_cast<float*>(smem), wave, lane, m0 + wm * WM, n0 + wn * WN);
+}
+
+// bf16 activations: both tiles go global -> LDS directly (16-byte LDS-DMA loads, no register
+// staging), two LDS stages, one barrier per 64-wide K step.  A DMA instruction fills 1 KB of LDS
+// in lane order, i.e. 8 rows x 128 bytes; each lane picks the k piece that belongs in its slot,
+// so the tile is stored with piece p of row r at slot p ^ ((r / 2) % 8), which makes the
+// 16-row MFMA fragment reads conflict-free.  Rows past M are clamped to M - 1 (they feed only
+// output rows that are never stored), so every load is unconditional.
+// One 16-byte-per-lane LDS-DMA load: lane l's 16 bytes from g land at l_base + 16 * l.
+__device__ __forceinline__ void lds_dma16(const bf16_t* g, bf16_t* l_base) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l_base, 16, 0, 0);
+}
+
+template <typename OT, int EPI, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(GemmArgs p) {
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int WAVES_N = BN / WN;
+  constexpr int NW = (BM / WM) * (BN / WN);
+  constexpr int STAGE = (BM + BN) * BK;              // bf16 per stage
+  constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;  // DMA instructions per wave per stage
+  static_assert(IA * NW * 8 == BM && IB * NW * 8 == BN, "tile rows must split into 8-row DMA groups");
+  extern __shared__ __align__(16) unsigned char smem[];
+  bf16_t* lds = reinterpret_cast<bf16_t*>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
+  const int total = nm * nn;
+  int id = blockIdx.x;
+  if ((total & 7) == 0) id = (id & 7) * (total >> 3) + (id >> 3);
+  constexpr int G = 8;
+  const int group = id / (G * nn);
+  const int first_m = group * G;
+  const int gsize = min(nm - first_m, G);
+  const int within = id % (G * nn);
+  const int tile_m = first_m + within % gsize;
+  const int tile_n = within / gsize;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
+
+  // DMA sources: lane l of a group fills row 8q + l/8, slot l%8 with piece (l%8) ^ ((row/2)%8)
+  const bf16_t* A = reinterpret_cast<const bf16_t*>(p.A);
+  const int lrow = lane >> 3, lslot = lane & 7;
+  const bf16_t* asrc[IA];
+  const bf16_t* bsrc[IB];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * WM + i * 16 + er + r;
-      if (m >= p.M) continue;
-      if constexpr (EPI == EPI_SWIGLU) {
-        // W rows interleaved in blocks of 8: columns 0-7 of each 16-wide tile are gate outputs,
-        // 8-15 the matching up outputs, held by lanes 8 apart
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const float g = acc[i][j][r], u = __shfl_xor(acc[i][j][r], 8, 64);
-          if (ec < 8) {
-            const int oc = ((n0 + wn * WN + j * 16) >> 1) + ec;
-            reinterpret_cast<OT*>(p.out)[(size_t)m * p.ldo + oc] = from_f<OT>(silu(g) * u);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int n = n0 + wn * WN + j * 16 + ec;
-          float v = acc[i][j][r];
-          if (p.bias) v += bf2f(p.bias[n]);
-          if constexpr (EPI == EPI_STORE) {
-            reinterpret_cast<OT*>(p.out)[(size_t)m * p.ldo + n] = from_f<OT>(v);
-          } else if constexpr (EPI == EPI_GELU) {
-            reinterpret_cast<OT*>(p.out)[(size_t)m * p.ldo + n] = from_f<OT>(gelu_erf(v));
-          } else if constexpr (EPI == EPI_RESID) {
-            float* o = reinterpret_cast<float*>(p.out) + (size_t)m * p.ldo + n;
-            *o = *o + v;
-          } else if constexpr (EPI == EPI_POS) {
-            float* o = reinterpret_cast<float*>(p.out) + (size_t)m * p.ldo + n;
-            *o = v + bf2f(p.pos[(size_t)(m % p.pos_rows) * p.N + n]);
-          }
-        }
-      }
-    }
+  for (int t = 0; t < IA; ++t) {
+    const int r = (wave * IA + t) * 8 + lrow;
+    asrc[t] = A + (size_t)min(m0 + r, p.M - 1) * p.lda + 8 * (lslot ^ ((r >> 1) & 7));
   }
+#pragma unroll
+  for (int t = 0; t < IB; ++t) {
+    const int r = (wave * IB + t) * 8 + lrow;
+    bsrc[t] = p.W + (size_t)(n0 + r) * p.ldw + 8 * (lslot ^ ((r >> 1) & 7));
+  }
+  auto dma = [&](int kt, int stage) {
+    bf16_t* a = lds + stage * STAGE;
+    bf16_t* b = a + BM * BK;
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int t = 0; t < IA; ++t)
+      lds_dma16(asrc[t] + k0, a + (wave * IA + t) * 8 * BK);
+#pragma unroll
+    for (int t = 0; t < IB; ++t)
+      lds_dma16(bsrc[t] + k0, b + (wave * IB + t) * 8 * BK);
+  };
+
+  f32x4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // fragment reads: row fr of a 16-row block, k piece 4s + fk of the 64-wide step; the block
+  // base is a multiple of 16 rows, so the swizzle depends on fr only
+  const int fr = lane & 15, fk = lane >> 4;
+  const int sw = (fr >> 1) & 7;
+  const int off0 = fr * BK + 8 * (fk ^ sw);          // elements, sub-step 0
+  const int off1 = fr * BK + 8 * ((fk + 4) ^ sw);    // sub-step 1
+  const int nk = p.K / BK;
+  dma(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const bf16_t* a = lds + (kt & 1) * STAGE + wm * WM * BK;
+    const bf16_t* b = lds + (kt & 1) * STAGE + BM * BK + wn * WN * BK;
+    Frag8 fa[2][TM], fb[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      fa[0][i] = *reinterpret_cast<const Frag8*>(a + i * 16 * BK + off0);
+      fa[1][i] = *reinterpret_cast<const Frag8*>(a + i * 16 * BK + off1);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      fb[0][j] = *reinterpret_cast<const Frag8*>(b + j * 16 * BK + off0);
+      fb[1][j] = *reinterpret_cast<const Frag8*>(b + j * 16 * BK + off1);
+    }
+    // the next stage's DMA is issued after this stage's reads, so that no read has to wait for it
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < nk) dma(kt + 1, (kt + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(fa[s][i], fb[s][j], acc[i][j]);
+    // every wave's DMA has landed (and every read of the other stage is done) before anyone goes
+    // on; the scheduling barrier keeps the MFMAs above the wait, which the compiler would
+    // otherwise hoist (they touch no memory) and so serialise the DMA with the compute
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+
+  gemm_epilogue<OT, EPI, WM, WN>(p, acc, reinterpret_cast<float*>(smem), wave, lane, m0 + wm * WM, n0 + wn * WN);
 }
 
 template <typename TA, typename OT, int EPI, int BM, int BN, int WM, int WN>
 static hipError_t launch_tile(const GemmArgs& p, hipStream_t s) {
   constexpr bool F32A = sizeof(TA) == 4;
   const size_t lds = (size_t)2 * (BM * LDK * (F32A ? 2 : 1) + BN * LDK) * sizeof(bf16_t);
+  static_assert((size_t)(BM / WM) * (BN / WN) * 16 * (WN + 4) * 4 <=
+                (size_t)2 * (BM * LDK + BN * LDK) * sizeof(bf16_t), "epilogue scratch exceeds the tile buffers");
   auto kern = gemm_kernel<TA, OT, EPI, BM, BN, WM, WN>;
+  static bool attr_set = false;   // benign race: idempotent attribute
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
+  hipLaunchKernelGGL(kern, dim3(nm * nn), dim3((BM / WM) * (BN / WN) * 64), lds, s, p);
+  return hipGetLastError();
+}
+
+template <typename OT, int EPI, int BM, int BN, int WM, int WN>
+static hipError_t launch_dma(const GemmArgs& p, hipStream_t s) {
+  constexpr size_t lds = (size_t)2 * (BM + BN) * BK * sizeof(bf16_t);
+  static_assert((size_t)(BM / WM) * (BN / WN) * 16 * (WN + 4) * 4 <= lds, "epilogue scratch exceeds the stages");
+  auto kern = gemm_dma_kernel<OT, EPI, BM, BN, WM, WN>;
   static bool attr_set = false;   // benign race: idempotent attribute
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -208,7 +400,8 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   // two tiles per CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU).
   if constexpr (sizeof(TA) == 2) {
     const long tiles = (long)((p.M + 255) / 256) * (p.N / 256);
-    if (p.N % 256 == 0 && p.N >= 3072 && tiles >= 512) return launch_tile<TA, OT, EPI, 256, 256, 64, 128>(p, s);
+    if (p.N % 256 == 0 && p.N >= 3072 && tiles >= 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
+    return launch_dma<OT, EPI, 128, 128, 64, 64>(p, s);
   }
   return launch_tile<TA, OT, EPI, 128, 128, 64, 64>(p, s);
 }
@@ -216,7 +409,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
 template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
-  if (p.N % 128 || p.K % BK || p.lda % 8 || p.ldw % 8) return hipErrorInvalidValue;
+  if (p.N % 128 || p.K % BK || p.lda % 8 || p.ldw % 8 || p.ldo % 4) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_STORE: return launch_epi<TA, OT, EPI_STORE>(p, s);
     case EPI_GELU: return launch_epi<TA, OT, EPI_GELU>(p, s);
