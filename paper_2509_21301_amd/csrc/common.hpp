@@ -14,14 +14,16 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 NOVA_DEV float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
 
-// float -> bf16, round to nearest even (inputs are finite).
-NOVA_DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
-NOVA_DEV uint32_t pack2(float a, float b) { return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16); }
+// float -> bf16, round to nearest even (gfx950 converts in hardware, v_cvt_pk_bf16_f32).
+NOVA_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+
+// Two floats -> two bf16 in one dword (a in the low half), one conversion instruction.
+NOVA_DEV uint32_t pack2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
 
 // Activation element types: bf16 (storage bf16_t) or fp32.
 template <typename T> NOVA_DEV float to_f(T v);

@@ -10,7 +10,8 @@
 //    rescale is per lane;
 //  * O^T = V^T P^T with the same MFMA: the probabilities already sit in the B-operand layout,
 //    because an MFMA fragment's k index only has to agree between its A and B operands;
-//    V is therefore stored transposed by the projection kernel;
+//    V is therefore stored transposed by the projection kernel, and each V^T tile row is
+//    stored with two 4-key blocks of every 16 swapped so that a fragment is one 16-byte read;
 //  * head_dim 64 / 80 / 128 (80 = 5 k-steps of 16 for QK^T; PV pads the output rows to 96);
 //  * fp32 mode (tiny-stack exact mode): q, k, v, p are split into bf16 hi + lo parts and the
 //    three significant cross products are accumulated.
@@ -29,7 +30,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   constexpr int DP = (D + 31) / 32 * 32;    // output rows padded to 32
   constexpr int NC = DP / 32;               // output row blocks
   constexpr int KP = D + 8;                 // LDS pitch of K rows (bf16)
-  constexpr int VP = AK + 4;                // LDS pitch of V^T rows (bf16)
+  constexpr int VP = AK + 8;                // LDS pitch of V^T rows (bf16, 16-byte aligned rows)
   constexpr int NPART = F32 ? 2 : 1;
   __shared__ __align__(16) bf16_t ks[NPART][AK * KP];
   __shared__ __align__(16) bf16_t vs[NPART][DP * VP];
@@ -72,25 +73,26 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   constexpr int V_CH = D * AK / EPC;
   constexpr int K_IT = (K_CH + 255) / 256, V_IT = (V_CH + 255) / 256;
   u32x4 rk[K_IT], rv[V_IT];
+  // loads are unconditional (chunk index and key row clamped) so that the waits for them stay
+  // exact; the surplus chunks are never stored and keys past sk are masked
   auto load_tile = [&](int kv0) {
 #pragma unroll
     for (int i = 0; i < K_IT; ++i) {
-      const int c = tid + i * 256;
-      rk[i] = u32x4{0u, 0u, 0u, 0u};
-      if (c < K_CH) {
-        const int r = c / (D / EPC), col = (c % (D / EPC)) * EPC;
-        if (kv0 + r < p.sk) rk[i] = *reinterpret_cast<const u32x4*>(K + (size_t)(kv0 + r) * p.k_row + col);
-      }
+      const int c = min(tid + i * 256, K_CH - 1);
+      const int r = c / (D / EPC), col = (c % (D / EPC)) * EPC;
+      rk[i] = *reinterpret_cast<const u32x4*>(K + (size_t)min(kv0 + r, p.sk - 1) * p.k_row + col);
     }
 #pragma unroll
     for (int i = 0; i < V_IT; ++i) {
-      const int c = tid + i * 256;
-      if (c < V_CH) {
-        const int r = c / (AK / EPC), col = (c % (AK / EPC)) * EPC;
-        rv[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)r * p.sk_pad + kv0 + col);
-      }
+      const int c = min(tid + i * 256, V_CH - 1);
+      const int r = c / (AK / EPC), col = (c % (AK / EPC)) * EPC;
+      rv[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)r * p.sk_pad + kv0 + col);
     }
   };
+  // V^T tiles keep each row's keys in groups of 16 with the middle two 4-key blocks swapped
+  // (block b at position 2 (b % 2) + b / 2): the 8 keys a lane's P fragment covers, 4 at 4g and 4
+  // at 8 + 4g, then sit side by side and the A fragment is one 16-byte read
+  auto vpos = [](int key) { const int b = (key >> 2) & 3; return (key & ~15) + 4 * (((b & 1) << 1) | (b >> 1)); };
   auto store_tile = [&]() {
 #pragma unroll
     for (int i = 0; i < K_IT; ++i) {
@@ -121,13 +123,13 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
           bf16_t hh[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) hh[j] = f2bf(x[j]);
-          *reinterpret_cast<uint2*>(&vs[0][r * VP + col]) =
+          *reinterpret_cast<uint2*>(&vs[0][r * VP + vpos(col)]) =
               make_uint2((uint32_t)hh[0] | ((uint32_t)hh[1] << 16), (uint32_t)hh[2] | ((uint32_t)hh[3] << 16));
-          *reinterpret_cast<uint2*>(&vs[1][r * VP + col]) =
+          *reinterpret_cast<uint2*>(&vs[1][r * VP + vpos(col)]) =
               make_uint2(pack2(x[0] - bf2f(hh[0]), x[1] - bf2f(hh[1])), pack2(x[2] - bf2f(hh[2]), x[3] - bf2f(hh[3])));
         } else {
-          *reinterpret_cast<uint2*>(&vs[0][r * VP + col]) = make_uint2(rv[i][0], rv[i][1]);
-          *reinterpret_cast<uint2*>(&vs[0][r * VP + col + 4]) = make_uint2(rv[i][2], rv[i][3]);
+          *reinterpret_cast<uint2*>(&vs[0][r * VP + vpos(col)]) = make_uint2(rv[i][0], rv[i][1]);
+          *reinterpret_cast<uint2*>(&vs[0][r * VP + vpos(col + 4)]) = make_uint2(rv[i][2], rv[i][3]);
         }
       }
     }
@@ -223,20 +225,14 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) ph.w[e] = pack2(sacc[kb][8 * t + 2 * e], sacc[kb][8 * t + 2 * e + 1]);
         }
-        const int key = kb * 32 + 16 * t + 4 * g;
+        const int kpos = kb * 32 + 16 * t + 8 * g;     // keys 16t + 4g + 0..3 and 16t + 8 + 4g + 0..3
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
           const int vrow = c * 32 + lq;
-          Frag8 va;
-          const uint2 lo = *reinterpret_cast<const uint2*>(&vs[0][vrow * VP + key]);
-          const uint2 hi = *reinterpret_cast<const uint2*>(&vs[0][vrow * VP + key + 8]);
-          va.w[0] = lo.x; va.w[1] = lo.y; va.w[2] = hi.x; va.w[3] = hi.y;
+          const Frag8 va = *reinterpret_cast<const Frag8*>(&vs[0][vrow * VP + kpos]);
           o[c] = mfma32(va, ph, o[c]);
           if constexpr (F32) {
-            Frag8 vl;
-            const uint2 lo2 = *reinterpret_cast<const uint2*>(&vs[1][vrow * VP + key]);
-            const uint2 hi2 = *reinterpret_cast<const uint2*>(&vs[1][vrow * VP + key + 8]);
-            vl.w[0] = lo2.x; vl.w[1] = lo2.y; vl.w[2] = hi2.x; vl.w[3] = hi2.y;
+            const Frag8 vl = *reinterpret_cast<const Frag8*>(&vs[1][vrow * VP + kpos]);
             o[c] = mfma32(vl, ph, o[c]);
             o[c] = mfma32(va, pl, o[c]);
           }
