@@ -203,6 +203,9 @@ int nova_make_cu_mask(int n_cus, int first_slot, uint32_t* mask);
 /* Give `stage` the CUs in cu_mask (mask_words 32-bit words, bit i = CU i as above) and return
  * in *out_stream a library-owned stream restricted to them (created with
  * hipExtStreamCreateWithCUMask on first use of that mask, default priority, then cached).
+ * A new mask's complement (when it keeps a CU on every XCD) gets its stream created right
+ * after it, so that a stage pair on complementary masks sits on different hardware dispatch
+ * pipes and runs concurrently; pairs of other masks carry no such guarantee.
  * Work enqueued afterwards on *out_stream starts only after everything previously enqueued on
  * the stage's prior partition stream (ordering across the switch, Sec. 3.4: partitions change
  * only between forward passes).  Host-synchronous; does not wait for the device.
