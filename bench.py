@@ -245,7 +245,7 @@ def main():
     ap.add_argument("--batch", type=int, default=8, help="images per encode pass (headline)")
     ap.add_argument("--no-sweep", action="store_true", help="skip CU-share curves and co-run")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--rates", type=float, nargs="+", default=[4.0], help="request rates (req/s) of the serving runs")
+    ap.add_argument("--rates", type=float, nargs="+", default=[2.0, 4.0], help="request rates (req/s) of the serving runs")
     ap.add_argument("--window", type=float, default=10.0, help="arrival window (s) of each serving run")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
     ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32"],
@@ -410,16 +410,25 @@ def main():
         log(f"Eq. 3 optimum: decode {pv} CUs beside encode, {pp} beside prefill, expected E2E {lat:.3f} s")
         # serving: Poisson bursts through the Alg. 1 policy, co-run partitions vs time slicing
         serving = []
+        result["rate_optimum"] = []
         for rate in args.rates:
-            for mode, kw in [("nova_static", dict(mode="nova", decode_cus=(pv, pp))),
+            # the Pareto point for this rate: Eq. 1 plus the Eq. 6 queueing delay of encode + prefill
+            rv, rp, rlat = sched.best_under_load(curves, out_len, rate)
+            result["rate_optimum"].append({"rate_req_s": rate, "decode_cus_with_encode": rv,
+                                           "decode_cus_with_prefill": rp, "expected_e2e_s": round(rlat, 4)})
+            log(f"rate {rate}: Eq. 1 + Eq. 6 optimum decode {rv} CUs beside encode, {rp} beside prefill, "
+                f"expected E2E {rlat:.3f} s")
+            for mode, kw in [("nova_eq3_static", dict(mode="nova", decode_cus=(pv, pp))),
+                             ("nova_rate_static", dict(mode="nova", decode_cus=(rv, rp))),
                              ("nova_adaptive", dict(mode="nova", decode_cus=(pv, pp), alpha=32, minimum=32)),
                              ("time_sliced", dict(mode="time_sliced")),
                              ("multi_stream", dict(mode="multi_stream"))]:
                 trace = serve.poisson_trace(rate, args.window, seed=3)
                 res = srv.serve(kw, trace)
-                res.update({"mode": mode, "rate_req_s": rate, "window_s": args.window})
+                res.update({"mode": mode, "rate_req_s": rate, "window_s": args.window,
+                            "decode_cus": list(kw.get("decode_cus", (256, 256)))})
                 serving.append(res)
-                log(f"serve {mode:13s} rate {rate}: max E2E {res['max_e2e_s']:.3f} s, avg {res['avg_e2e_s']:.3f} s, "
+                log(f"serve {mode:16s} rate {rate}: max E2E {res['max_e2e_s']:.3f} s, avg {res['avg_e2e_s']:.3f} s, "
                     f"avg TBT {res['avg_tbt_ms']:.1f} ms, {res['throughput_req_s']:.2f} req/s")
         result["serving"] = serving
 

@@ -205,7 +205,9 @@ int nova_make_cu_mask(int n_cus, int first_slot, uint32_t* mask);
  * hipExtStreamCreateWithCUMask on first use of that mask, default priority, then cached).
  * A new mask's complement (when it keeps a CU on every XCD) gets its stream created right
  * after it, so that a stage pair on complementary masks sits on different hardware dispatch
- * pipes and runs concurrently; pairs of other masks carry no such guarantee.
+ * pipes and runs concurrently; pairs of other masks carry no such guarantee.  Stages given the
+ * same partial mask share its stream; the whole-GPU mask has a separate stream per stage
+ * (the three are created together).
  * Work enqueued afterwards on *out_stream starts only after everything previously enqueued on
  * the stage's prior partition stream (ordering across the switch, Sec. 3.4: partitions change
  * only between forward passes).  Host-synchronous; does not wait for the device.

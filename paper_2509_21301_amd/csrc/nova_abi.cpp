@@ -47,6 +47,7 @@ struct Global {
   int cus = 0;
   std::mutex mu;
   std::map<std::vector<uint32_t>, hipStream_t> mask_streams;   // partition stream pool
+  hipStream_t full_streams[3] = {nullptr, nullptr, nullptr};   // whole-GPU mask, one per stage
   hipStream_t stage_stream[3] = {nullptr, nullptr, nullptr};
   hipEvent_t stage_switch[3] = {nullptr, nullptr, nullptr};
   // timing
@@ -115,6 +116,10 @@ extern "C" int nova_init(int device) {
 extern "C" void nova_shutdown(void) {
   std::lock_guard<std::mutex> lk(g.mu);
   for (auto& kv : g.mask_streams) hipStreamDestroy(kv.second);
+  for (auto& fs : g.full_streams) {
+    if (fs) hipStreamDestroy(fs);
+    fs = nullptr;
+  }
   g.mask_streams.clear();
   for (int i = 0; i < 3; ++i) {
     if (g.stage_switch[i]) hipEventDestroy(g.stage_switch[i]);
@@ -758,8 +763,20 @@ extern "C" int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int 
   }
   std::lock_guard<std::mutex> lk(g.mu);
   hipStream_t ns;
-  auto it = g.mask_streams.find(m);
-  if (it == g.mask_streams.end()) {
+  // the whole-GPU mask is the one two stages may hold at once (a stage keeps a pass's stream
+  // until the pass ends): it gets one stream per stage, created together
+  bool full = true;
+  for (int w = 0; w < 8; ++w) full = full && m[w] == 0xFFFFFFFFu;
+  if (full) {
+    if (!g.full_streams[stage]) {
+      for (int st = 0; st < 3; ++st) {
+        if (g.full_streams[st]) continue;
+        hipError_t e = hipExtStreamCreateWithCUMask(&g.full_streams[st], 8, m.data());
+        if (e != hipSuccess) return fail(NOVA_EHIP, "hipExtStreamCreateWithCUMask: %s", hipGetErrorString(e));
+      }
+    }
+    ns = g.full_streams[stage];
+  } else if (g.mask_streams.find(m) == g.mask_streams.end()) {
     hipError_t e = hipExtStreamCreateWithCUMask(&ns, 8, m.data());
     if (e != hipSuccess) return fail(NOVA_EHIP, "hipExtStreamCreateWithCUMask: %s", hipGetErrorString(e));
     g.mask_streams[m] = ns;
@@ -783,7 +800,7 @@ extern "C" int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int 
       g.mask_streams[c] = cs;
     }
   } else {
-    ns = it->second;
+    ns = g.mask_streams[m];
   }
   hipStream_t old = g.stage_stream[stage];
   if (old && old != ns) {

@@ -1,7 +1,8 @@
 """Partition planning for co-running stages (the paper's Sec. 3.3): expected end-to-end latency
 of an ideal pipeline (Eq. 1-2), the enumeration of the best static partition (Eq. 3), the
-throughput approximation (Eq. 4), the latency-throughput Pareto front, and the adaptive decode
-share (Eq. 5), all driven by measured per-stage curves.
+throughput approximation (Eq. 4), the latency-throughput Pareto front, the adaptive decode
+share (Eq. 5), and the choice of a Pareto point for a request rate using the M/G/1 queueing
+delay of the encode + prefill server (Eq. 6), all driven by measured per-stage curves.
 
 A partition here is the number of CUs the decode stage holds while it co-runs with vision
 encode (P_v) or with prefill (P_p); the co-running stage holds the rest of the 256.  On
@@ -74,6 +75,29 @@ def pareto_front(c: StageCurves, out_len: float):
             front.append(p)
             best_thr = p[1]
     return front
+
+
+def queue_wait(t_service: float, rate: float) -> float:
+    """Eq. 6 for a service time that is the same for every request (E[T^2] = T^2): the expected
+    wait in the vision queue at `rate` requests/s; infinite when the server is saturated."""
+    rho = rate * t_service
+    return float("inf") if rho >= 1.0 else rate * t_service * t_service / (2.0 * (1.0 - rho))
+
+
+def best_under_load(c: StageCurves, out_len: float, rate: float):
+    """The partition pair minimising Eq. 1 plus the Eq. 6 queueing delay at `rate` (the Pareto
+    point the request rate calls for: fewer decode CUs as the rate grows).  Returns
+    (P_v, P_p, latency); when every pair saturates, the pair of highest throughput (Eq. 4)."""
+    best = None
+    for pv in c.shares:
+        for pp in c.shares:
+            lat = expected_e2e(c, pv, pp, out_len) + queue_wait(c.t_vision[pv] + c.t_prefill[pp], rate)
+            if best is None or lat < best[2]:
+                best = (pv, pp, lat)
+    if best[2] == float("inf"):
+        pv, pp = max(((a, b) for a in c.shares for b in c.shares), key=lambda ab: ideal_throughput(c, *ab))
+        best = (pv, pp, float("inf"))
+    return best
 
 
 def decode_cus(n_pending: int, optimum: int, alpha: int, minimum: int, granule: int = GRANULE) -> int:

@@ -132,12 +132,16 @@ class Server:
         s.synchronize()
         req.t_vis1 = time.perf_counter()
 
+    # Host <-> device copies go on the stage's own stream: torch's default stream is HIP's null
+    # stream, which waits for every other (blocking) stream, so a copy there would hold one
+    # stage until the co-running stage's pass ends.
     def _prefill(self, req):
         s = self._stream(nova.STAGE_PREFILL)
-        tbl = torch.from_numpy(req.table_row).to("cuda", non_blocking=False)
-        nxt = self.llm.prefill(self.vis_buf[0], req.ids, tbl, self.kv, stream=s)
-        s.synchronize()
-        req.last_token = int(nxt.item())
+        with torch.cuda.stream(s):
+            tbl = torch.from_numpy(req.table_row).to("cuda", non_blocking=False)
+            nxt = self.llm.prefill(self.vis_buf[0], req.ids, tbl, self.kv, stream=s)
+            s.synchronize()
+            req.last_token = int(nxt.item())
         req.t_pre1 = time.perf_counter()
 
     def _decode_step(self, batch):
@@ -149,10 +153,10 @@ class Server:
         max_ctx = int(pos.max()) + 1
         with torch.cuda.stream(s):
             ids_d, pos_d, tab_d = ids.cuda(non_blocking=True), pos.cuda(non_blocking=True), tab.cuda(non_blocking=True)
-        nxt = self.llm.decode(ids_d, pos_d, tab_d, self.kv, max_ctx, stream=s)
-        s.synchronize()
-        now = time.perf_counter()
-        out = nxt.cpu()
+            nxt = self.llm.decode(ids_d, pos_d, tab_d, self.kv, max_ctx, stream=s)
+            s.synchronize()
+            now = time.perf_counter()
+            out = nxt.cpu()
         for r, t in zip(batch, out.tolist()):
             r.last_token = t
             r.t_tokens.append(now)

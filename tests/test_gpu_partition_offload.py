@@ -4,7 +4,7 @@
   their shader engines, disjoint from the complementary mask, and full masks see all 256 CUs.
 * Work switched between partition streams keeps its order (decode steps that read the KV
   written by the previous step on another partition give bit-identical logits).
-* Invalid masks are rejected.
+* Invalid masks are rejected; the whole-GPU mask has a stream per stage.
 * Encoding with K = 2 or 3 device slots streamed from pinned memory (including a deliberately
   delayed preload) is bit-identical to the resident model, across consecutive calls whose ring
   wraps into the next pass; the encoder with 2x2 merge matches the oracle.
@@ -20,6 +20,20 @@ pytestmark = pytest.mark.gpu
 
 VIT5 = synth.VitConfig(hidden=256, heads=4, mlp=1024, layers=5, patch=4, merge=2, out_hidden=256,
                        image_h=32, image_w=48, name="vit5_merge")
+
+
+def test_whole_gpu_mask_has_a_stream_per_stage(gpu_lib):
+    # two stages may both hold the whole GPU for a pass; sharing one stream would queue one
+    # stage's pass behind the other's
+    nova = gpu_lib
+    full = [0xFFFFFFFF] * 8
+    streams = {nova.set_stage_partition(st, full).cuda_stream
+               for st in (nova.STAGE_ENCODE, nova.STAGE_PREFILL, nova.STAGE_DECODE)}
+    assert len(streams) == 3
+    a = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(96, 0)).cuda_stream
+    b = nova.set_stage_partition(nova.STAGE_ENCODE, nova.make_cu_mask(96, 0)).cuda_stream
+    assert a == b                      # a partial mask is one stream, whoever holds it
+    assert nova.set_stage_partition(nova.STAGE_DECODE, full).cuda_stream in streams
 
 
 def test_partition_streams_stay_on_their_cus(gpu_lib):

@@ -56,3 +56,21 @@ def test_from_corun_records():
             {"pair": "decode+prefill", "decode_cus": 64, "prefill_ms_corun": 56.0, "decode_step_ms_corun": 12.5}]
     c = sched.StageCurves.from_corun(recs)
     assert c.shares == [64] and c.t_vision[64] == 0.05 and c.t_dec_prefill[64] == 0.0125
+
+
+def test_best_under_load_matches_eq1_plus_eq6():
+    c = curves(3)
+    for rate in (0.5, 2.0, 5.0):
+        pv, pp, lat = sched.best_under_load(c, 32, rate)
+        ref = []
+        for a in SHARES:
+            for b in SHARES:
+                t = c.t_vision[a] + c.t_prefill[b]
+                w = osched.mg1_wait(rate, t, t * t) if rate * t < 1 else float("inf")
+                ref.append((osched.e2e_latency(c.t_vision[a], c.t_prefill[b], c.t_dec_vision[a], c.t_dec_prefill[b], 32) + w, a, b))
+        r = min(ref)
+        assert (pv, pp) == (r[1], r[2]) and abs(lat - r[0]) < 1e-12
+    # a higher rate never hands decode more CUs in total
+    lo, hi = sched.best_under_load(c, 32, 0.1), sched.best_under_load(c, 32, 6.0)
+    assert hi[0] + hi[1] <= lo[0] + lo[1]
+    assert sched.queue_wait(0.2, 5.0) == float("inf")
