@@ -271,7 +271,9 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   const int total = nm * nn;
   int id = blockIdx.x;
   if ((total & 7) == 0) id = (id & 7) * (total >> 3) + (id >> 3);
-  constexpr int G = 8;
+  // groups of G M-tiles sweep the N tiles together (an XCD's ~32 resident tiles then share a few
+  // A and W panels in its L2); measured best at 16 for 256-row tiles and 8 for 128-row tiles
+  constexpr int G = BM >= 256 ? 16 : 8;
   const int group = id / (G * nn);
   const int first_m = group * G;
   const int gsize = min(nm - first_m, G);
@@ -396,11 +398,11 @@ static hipError_t launch_dma(const GemmArgs& p, hipStream_t s) {
 
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
-  // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when N is wide and there are at least
-  // two tiles per CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU).
+  // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when there are at least two tiles per
+  // CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU).
   if constexpr (sizeof(TA) == 2) {
     const long tiles = (long)((p.M + 255) / 256) * (p.N / 256);
-    if (p.N % 256 == 0 && p.N >= 3072 && tiles >= 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
+    if (p.N % 256 == 0 && tiles >= 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     return launch_dma<OT, EPI, 128, 128, 64, 64>(p, s);
   }
   return launch_tile<TA, OT, EPI, 128, 128, 64, 64>(p, s);
