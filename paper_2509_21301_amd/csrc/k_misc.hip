@@ -10,35 +10,39 @@
 namespace nova {
 
 // ------------------------------------------------------------------ norms (one wave per row)
+// LayerNorm (ln = 1, with shift) or RMSNorm (ln = 0) of fp32 rows of width H <= 4096: the row is
+// read once into registers (lane l holds float4 l, l + 64, ...), mean and variance come from the
+// registers (two passes over them, so the variance is well conditioned), and each lane writes 4
+// outputs at a time.  merge > 1 scatters row (image, py, px) of a gh x gw patch grid to the
+// merged token it belongs to, at column block (py % merge) * merge + px % merge.
+constexpr int NORM_MAXV = 16;     // float4 per lane: H <= 64 * 4 * 16
 template <typename T>
-__global__ void norm_kernel(const float* __restrict__ x, int M, int H, const bf16_t* __restrict__ g,
-                            const bf16_t* __restrict__ bb, float eps, int ln, T* __restrict__ out, int ldo,
-                            int merge, int gh, int gw) {
+__global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, int M, int H, const bf16_t* __restrict__ g,
+                                                   const bf16_t* __restrict__ bb, float eps, int ln, T* __restrict__ out,
+                                                   int ldo, int merge, int gh, int gw) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
   const float4* xr = reinterpret_cast<const float4*>(x + (size_t)row * H);
   const int n4 = H / 4;
-  float s = 0.f, ss = 0.f;
-  for (int i = lane; i < n4; i += 64) {
-    float4 v = xr[i];
-    s += v.x + v.y + v.z + v.w;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  float4 v[NORM_MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NORM_MAXV; ++j) {
+    const int i = j * 64 + lane;
+    v[j] = i < n4 ? xr[i] : float4{0.f, 0.f, 0.f, 0.f};
+    s += v[j].x + v[j].y + v[j].z + v[j].w;
   }
-  s = wave_sum(s);
-  float mean = 0.f, rstd;
-  if (ln) {
-    mean = s / H;
-    float vs = 0.f;   // second pass for a well-conditioned variance
-    for (int i = lane; i < n4; i += 64) {
-      float4 v = xr[i];
-      float a = v.x - mean, b = v.y - mean, c = v.z - mean, d = v.w - mean;
-      vs += a * a + b * b + c * c + d * d;
+  const float mean = ln ? wave_sum(s) / H : 0.f;
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NORM_MAXV; ++j) {
+    if (j * 64 + lane < n4) {
+      const float a = v[j].x - mean, b = v[j].y - mean, c = v[j].z - mean, d = v[j].w - mean;
+      ss += a * a + b * b + c * c + d * d;
     }
-    rstd = rsqrtf(wave_sum(vs) / H + eps);
-  } else {
-    rstd = rsqrtf(wave_sum(ss) / H + eps);
   }
+  const float rstd = rsqrtf(wave_sum(ss) / H + eps);
   size_t orow = row, ocol = 0;
   if (merge > 1) {
     const int per_img = gh * gw;
@@ -47,15 +51,22 @@ __global__ void norm_kernel(const float* __restrict__ x, int M, int H, const bf1
     ocol = (size_t)((py % merge) * merge + px % merge) * H;
   }
   T* o = out + orow * ldo + ocol;
-  for (int i = lane; i < n4; i += 64) {
-    float4 v = xr[i];
-    float y[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = 4 * i + j;
-      float t = (y[j] - mean) * rstd * bf2f(g[c]);
-      if (ln) t += bf2f(bb[c]);
-      o[c] = from_f<T>(t);
+  for (int j = 0; j < NORM_MAXV; ++j) {
+    const int i = j * 64 + lane;
+    if (i >= n4) continue;
+    const uint2 gg = *reinterpret_cast<const uint2*>(g + 4 * i);
+    float y[4] = {(v[j].x - mean) * rstd * bf2f((bf16_t)(gg.x & 0xffff)), (v[j].y - mean) * rstd * bf2f((bf16_t)(gg.x >> 16)),
+                  (v[j].z - mean) * rstd * bf2f((bf16_t)(gg.y & 0xffff)), (v[j].w - mean) * rstd * bf2f((bf16_t)(gg.y >> 16))};
+    if (ln) {
+      const uint2 b2 = *reinterpret_cast<const uint2*>(bb + 4 * i);
+      y[0] += bf2f((bf16_t)(b2.x & 0xffff)); y[1] += bf2f((bf16_t)(b2.x >> 16));
+      y[2] += bf2f((bf16_t)(b2.y & 0xffff)); y[3] += bf2f((bf16_t)(b2.y >> 16));
+    }
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4*>(o + 4 * i) = float4{y[0], y[1], y[2], y[3]};
+    } else {
+      *reinterpret_cast<uint2*>(o + 4 * i) = make_uint2(pack2(y[0], y[1]), pack2(y[2], y[3]));
     }
   }
 }
@@ -64,7 +75,7 @@ template <typename T>
 hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln, T* out,
                      int ldo, int merge, int gh, int gw, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (H % 4) return hipErrorInvalidValue;
+  if (H % 4 || H > 4 * 64 * NORM_MAXV || ldo % 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL((norm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, g, b, eps, ln, out, ldo, merge, gh, gw);
   return hipGetLastError();
 }
@@ -117,30 +128,40 @@ __global__ void rope_inplace_kernel(T* __restrict__ qkv, int rows, int S, int n_
   }
 }
 
-// V transpose for attention (and the paged K/V cache writes): one workgroup per
-// (64-token tile, kv head, batch).  V rows go through LDS so that V^T rows are written whole.
+// ------------------------------------------------------------------ V transpose and paged K/V append
+// V of the projected rows -> V^T [b][kv head][D][sk_pad] (keys past S zero) for the attention
+// kernel, and for a paged cache K [blk][kvh][slot][D], V [blk][kvh][D][slot].  A block moves 64
+// tokens of one kv head through an LDS tile: 16-byte reads of each token's D values, 16-byte
+// writes of 16 / sizeof(T) consecutive keys of each V^T row.
 template <typename T>
 __global__ void __launch_bounds__(256) kv_scatter_kernel(const T* __restrict__ qkv, int S, int n_q, int n_kv, int D,
                                                         T* __restrict__ vt, int sk_pad, T* __restrict__ kpool,
                                                         T* __restrict__ vpool, const int* __restrict__ table, int block) {
-  __shared__ float tile[64][129];
+  constexpr int EPC = 16 / sizeof(T);      // elements per 16-byte chunk
+  constexpr int TP = 128 + EPC;            // tile pitch (elements), D <= 128
+  __shared__ __align__(16) T tile[64 * TP];
   const int t0 = blockIdx.x * 64, kvh = blockIdx.y, b = blockIdx.z;
   const int ld = (n_q + 2 * n_kv) * D;
   const T* vsrc = qkv + (size_t)b * S * ld + (size_t)(n_q + n_kv) * D + (size_t)kvh * D;
   const T* ksrc = qkv + (size_t)b * S * ld + (size_t)n_q * D + (size_t)kvh * D;
-  for (int i = threadIdx.x; i < 64 * D; i += 256) {
-    const int t = i / D, c = i % D;
-    tile[t][c] = (t0 + t < S) ? to_f<T>(vsrc[(size_t)(t0 + t) * ld + c]) : 0.f;
+  const int cpr = D / EPC;
+  for (int c = threadIdx.x; c < 64 * cpr; c += 256) {
+    const int t = c / cpr, d0 = (c % cpr) * EPC;
+    u32x4 val = {0u, 0u, 0u, 0u};
+    if (t0 + t < S) val = *reinterpret_cast<const u32x4*>(vsrc + (size_t)(t0 + t) * ld + d0);
+    *reinterpret_cast<u32x4*>(tile + t * TP + d0) = val;
   }
   __syncthreads();
-  // V^T [b][kvh][D][sk_pad]; keys beyond S are zero
   T* vdst = vt + ((size_t)b * n_kv + kvh) * D * (size_t)sk_pad;
-  for (int i = threadIdx.x; i < 64 * D; i += 256) {
-    const int c = i / 64, t = i % 64;
-    if (t0 + t < sk_pad) vdst[(size_t)c * sk_pad + t0 + t] = from_f<T>(tile[t][c]);
+  constexpr int TCN = 64 / EPC;            // key chunks per V^T row of this block
+  for (int c = threadIdx.x; c < D * TCN; c += 256) {
+    const int d = c / TCN, tc = (c % TCN) * EPC;
+    T vals[EPC];
+#pragma unroll
+    for (int j = 0; j < EPC; ++j) vals[j] = tile[(tc + j) * TP + d];
+    *reinterpret_cast<u32x4*>(vdst + (size_t)d * sk_pad + t0 + tc) = *reinterpret_cast<const u32x4*>(vals);
   }
   if (table == nullptr) return;
-  // paged cache: K [blk][kvh][slot][D], V [blk][kvh][D][slot]
   for (int i = threadIdx.x; i < 64 * D; i += 256) {
     const int t = i / D, c = i % D;
     const int tok = t0 + t;
@@ -153,7 +174,7 @@ __global__ void __launch_bounds__(256) kv_scatter_kernel(const T* __restrict__ q
     const int tok = t0 + t;
     if (tok >= S) continue;
     const int phys = table[tok / block], slot = tok % block;
-    vpool[(((size_t)phys * n_kv + kvh) * D + c) * block + slot] = from_f<T>(tile[t][c]);
+    vpool[(((size_t)phys * n_kv + kvh) * D + c) * block + slot] = tile[t * TP + c];
   }
 }
 
@@ -161,7 +182,7 @@ template <typename T>
 hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0, T* vt,
                        int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s) {
   if (S <= 0) return hipSuccess;
-  if (D > 128 || sk_pad < S) return hipErrorInvalidValue;
+  if (D > 128 || D % 8 || sk_pad < S || sk_pad % 64) return hipErrorInvalidValue;
   const int ld = (n_q + 2 * n_kv) * D;
   if (rope_theta > 0.f) {
     const long total = (long)batch * S * (n_q + n_kv) * (D / 2);
@@ -171,7 +192,7 @@ hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  dim3 grid((sk_pad + 63) / 64, n_kv, batch);
+  dim3 grid(sk_pad / 64, n_kv, batch);
   hipLaunchKernelGGL((kv_scatter_kernel<T>), grid, dim3(256), 0, s, qkv, S, n_q, n_kv, D, vt, sk_pad, kpool, vpool,
                      table, block);
   return hipGetLastError();
