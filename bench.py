@@ -106,6 +106,27 @@ def decode_bytes(cfg, batch, ctx):
     return weights, kv
 
 
+# ----------------------------------------------------------------------------- HBM traffic
+def gemm_traffic():
+    """HBM bytes per GEMM launch of the encode pass, from the committed rocprofv3 PMC summary
+    (FETCH_SIZE and WRITE_SIZE, each scaled by its reading for a plain 1 GiB copy); None when the
+    summary is missing or the GEMM source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "encode_gemm_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2509_21301_amd", "csrc", "k_gemm.hip")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and line.strip().startswith("- `"):
+            k, v = line.strip()[3:].split("`", 1)
+            vals[k] = v.strip(" :`")
+    want = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if vals.get("kernel_source_sha256") != want or "traffic_bytes_per_launch" not in vals:
+        return None
+    return int(float(vals["traffic_bytes_per_launch"]))
+
+
 # ----------------------------------------------------------------------------- timing helpers
 def time_passes(torch, fn, reps, stream):
     torch.cuda.synchronize()
@@ -248,8 +269,9 @@ def main():
     ap.add_argument("--rates", type=float, nargs="+", default=[2.0, 4.0], help="request rates (req/s) of the serving runs")
     ap.add_argument("--window", type=float, default=10.0, help="arrival window (s) of each serving run")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
-    ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32"],
-                    help="run only this stage in a loop of --steps passes (for rocprofv3)")
+    ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32", "copy"],
+                    help="run only this stage in a loop of --steps passes (for rocprofv3); 'copy' is a plain "
+                         "1 GiB device copy that calibrates the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the method serves all three stages on a single GPU; "
@@ -259,6 +281,14 @@ def main():
     import torch
     from paper_2509_21301_amd import nova, sched, serve, synth
     device = "cuda"
+    if args.profile_stage == "copy":
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=device)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            dst.copy_(src)
+        ms = time_passes(torch, lambda: dst.copy_(src), args.steps, torch.cuda.current_stream())
+        log(f"copy 1 GiB: {ms:.3f} ms per pass, {2 * (1 << 30) / (ms / 1e3) / 1e9:.1f} GB/s (read + write)")
+        return
     nova.init(0)
     st = Stages(nova, torch, synth, device, args.batch)
     vc, lc = st.vc, st.lc
@@ -307,7 +337,8 @@ def main():
     flops_per_launch = fam_flops[dom] * args.steps / max(n_dom, 1)
     achieved = flops_per_launch / ((t_dom / max(n_dom, 1)) / 1e3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                "traffic": gemm_traffic() if dom == "gemm" else None,
                 "avg_launch_ms": round(t_dom / max(n_dom, 1), 4),
                 "flops_per_launch": flops_per_launch,
                 "other_kernels": {f: round(fam_flops[f] * args.steps / kinds[f][0] / 1e9, 1)
