@@ -12,9 +12,16 @@
 // the order they are consumed so that each wait covers only its own chunk.
 // When N alone gives too few workgroups, K is split and a small second pass reduces the fp32
 // partials and applies the epilogue; otherwise the epilogue is applied directly.
+// RMSNorm folding (small decode batches): a residual producer (O, down projection) writes the
+// updated residual x, x times the next norm's gain, and per-64-row-tile sums of squares of x;
+// with split-K the last split of each tile (a device-scope arrival counter; partials written
+// through to the coherent level, so no cache write-back is needed) folds the partials in.  The
+// consumer (QKV, gate/up, LM head) reads x * gain as X and scales output column b by
+// rsqrt(mean x_b^2 + eps), summing the tile parts in a fixed order.
 // The k index of an MFMA fragment only has to agree between its two operands, which leaves the
 // assignment of k pieces to lanes free.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -47,9 +54,13 @@ size_t gemv_partial_floats(int B, int N, int K, bool f32x) {
 // slot (k/8) ^ (row % 16).
 __device__ __forceinline__ int swz(int row, int piece) { return row * GV_KC + 8 * (piece ^ (row & 15)); }
 
-template <typename TX, typename OT, int NB, int EPI, bool DIRECT>
+// TA: activation type of X (bf16, or fp32 for the exact mode whose operands are split into bf16
+// hi + lo).  NSCALE: X holds x * gain of a folded RMSNorm; output columns are scaled by the row's
+// rsqrt(mean x^2 + eps), from the producer's per-tile sums of squares.
+template <typename TA, typename OT, int NB, int EPI, bool DIRECT, bool NSCALE>
 __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
-  constexpr bool F32X = sizeof(TX) == 4;
+  using TX = TA;
+  constexpr bool F32X = sizeof(TA) == 4;                  // X fp32, operands split into bf16 hi + lo
   constexpr int XROWS = 16 * NB;                          // batch rows held (B padded)
   constexpr int XR = F32X ? 1 : 2;                        // X ring slots
   constexpr int XSLOT = XROWS * GV_KC * (F32X ? 2 : 1);   // bf16 per slot (fp32 mode: hi, lo)
@@ -57,6 +68,8 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
   constexpr int XL = F32X ? 2 * XPT : XPT;                // X loads per thread per chunk
   __shared__ __align__(16) bf16_t wt[4][GV_RW * GV_KC];
   __shared__ __align__(16) bf16_t xs[XR * XSLOT];
+  __shared__ float red[EPI == EPI_RESID ? 4 : 1][32];     // per-wave row statistics (residual producers)
+  __shared__ float rstd_s[NSCALE ? 32 : 1];                // per-row RMSNorm scale (normalising consumers)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_base = blockIdx.x * GV_ROWS + wave * GV_RW;
@@ -152,12 +165,30 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
 
   // loads are unconditional (clamped at the tail) and issued in consumption order, so that the
   // wait before each use covers only its own chunk
+  // the row statistic first (ahead of the weight stream in the in-order load counter): wave w
+  // takes batch rows w, w + 4, ...; lane t holds tile part t (<= 64 parts), summed by a
+  // fixed-order butterfly
+  float ssv[NSCALE ? (16 * NB + 3) / 4 : 1];
+  if constexpr (NSCALE) {
+#pragma unroll
+    for (int i = 0; i < (16 * NB + 3) / 4; ++i) {
+      const int b = min(wave + 4 * i, p.B - 1);
+      ssv[i] = lane < p.ss_parts ? p.ss_in[(size_t)lane * p.B + b] : 0.f;
+    }
+  }
   WBuf w0, w1, w2;
   XBuf x0, x1, x2;
   load_x(0, x0);
   load_w(0, w0);
   load_x(1, x1);
   load_w(1, w1);
+  if constexpr (NSCALE) {
+#pragma unroll
+    for (int i = 0; i < (16 * NB + 3) / 4; ++i) {
+      const float ss = wave_sum(ssv[i]);
+      if (lane == 0 && wave + 4 * i < p.B) rstd_s[wave + 4 * i] = rsqrtf(ss / p.K + p.eps);
+    }
+  }
   store_x(x0, 0);
   __syncthreads();
   for (int c = 0; c < nchunks; c += 3) {
@@ -173,6 +204,14 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
   }
 
   // lane holds D[n = 4*(lane/16) + r][b = lane%16] of each 16x16 tile
+  if constexpr (NSCALE) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float rstd = rstd_s[min(j * 16 + (lane & 15), p.B - 1)];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[j][r] *= rstd;
+    }
+  }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int b = j * 16 + (lane & 15);
@@ -203,7 +242,13 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
     for (int r = 0; r < 4; ++r) {
       const int nr = (lane >> 4) * 4 + r;
       if constexpr (!DIRECT) {
-        if (b < p.B) p.partial[((size_t)split * p.B + b) * p.N + n_base + nr] = acc[j][r];
+        float* dst = p.partial + ((size_t)split * p.B + b) * p.N + n_base + nr;
+        if (EPI == EPI_RESID && p.counters != nullptr) {
+          // written through to the device-coherent level: the tile's last split reads them
+          if (b < p.B) __hip_atomic_store(dst, acc[j][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+          if (b < p.B) *dst = acc[j][r];
+        }
       } else if constexpr (EPI == EPI_SWIGLU) {
         // rows interleaved in blocks of 8: rows 0-7 of the tile are gate rows, 8-15 the matching
         // up rows, held by lanes 32 apart
@@ -213,10 +258,80 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
           reinterpret_cast<OT*>(p.out)[(size_t)b * p.ldo + oc] = from_f<OT>(silu(acc[j][r]) * up);
         }
       } else if constexpr (EPI == EPI_RESID) {
-        if (b < p.B) reinterpret_cast<float*>(p.out)[(size_t)b * p.ldo + n_base + nr] += acc[j][r];
+        if (b < p.B) {
+          float* o = reinterpret_cast<float*>(p.out) + (size_t)b * p.ldo + n_base + nr;
+          const float xn = *o + acc[j][r];
+          *o = xn;
+          if (p.gain_out != nullptr)
+            reinterpret_cast<TA*>(p.aout)[(size_t)b * p.ldao + n_base + nr] = from_f<TA>(xn * bf2f(p.gain_out[n_base + nr]));
+          acc[j][r] = xn * xn;         // kept for the row statistic below
+        } else {
+          acc[j][r] = 0.f;
+        }
       } else {
         if (b < p.B) reinterpret_cast<OT*>(p.out)[(size_t)b * p.ldo + n_base + nr] = from_f<OT>(acc[j][r]);
       }
+    }
+    if constexpr (EPI == EPI_RESID && DIRECT) {
+      // this wave's 16 rows of the updated residual, summed per batch row (lanes 16 apart share b)
+      float sq = acc[j][0] + acc[j][1] + acc[j][2] + acc[j][3];
+      sq += __shfl_xor(sq, 16, 64);
+      sq += __shfl_xor(sq, 32, 64);
+      if (lane < 16) red[wave][j * 16 + lane] = sq;
+    }
+  }
+  if constexpr (EPI == EPI_RESID && DIRECT) {
+    if (p.ss_out != nullptr) {       // the workgroup's 64 rows: the 4 waves in a fixed order
+      __syncthreads();
+      if (tid < p.B) p.ss_out[(size_t)blockIdx.x * p.B + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+    }
+  }
+  if constexpr (EPI == EPI_RESID && !DIRECT) {
+    if (p.counters != nullptr) {
+      // the last split to finish this workgroup's 64 rows folds every split's partials into the
+      // residual and writes the rows' sum of squares: each thread waits until its write-through
+      // partial stores have completed, then one device-scope counter increment per workgroup
+      // tells the splits apart; the last one reads the partials from the coherent level (no L2
+      // write-back or invalidate is needed)
+      __shared__ int last;
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (tid == 0)
+        last = __hip_atomic_fetch_add(p.counters + blockIdx.x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               gridDim.y - 1;
+      __syncthreads();
+      if (!last) return;
+      float* xo = reinterpret_cast<float*>(p.out);
+      const int n0 = blockIdx.x * GV_ROWS;
+      const float gn = p.gain_out != nullptr ? bf2f(p.gain_out[n0 + lane]) : 0.f;
+      // wave w takes batch rows w, w + 4, ... (at most 8); lane = row within the tile; all of a
+      // split's loads are issued before any is summed
+      constexpr int BPW = (16 * NB + 3) / 4;
+      float v[BPW];
+#pragma unroll
+      for (int i = 0; i < BPW; ++i) v[i] = 0.f;
+#pragma unroll 4
+      for (int sp = 0; sp < (int)gridDim.y; ++sp) {
+#pragma unroll
+        for (int i = 0; i < BPW; ++i) {
+          const int b = wave + 4 * i;
+          if (b < p.B)
+            v[i] += __hip_atomic_load(p.partial + ((size_t)sp * p.B + b) * p.N + n0 + lane, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < BPW; ++i) {
+        const int b = wave + 4 * i;
+        if (b >= p.B) break;             // uniform per wave
+        float* o = xo + (size_t)b * p.ldo + n0 + lane;
+        const float xn = *o + v[i];
+        *o = xn;
+        if (p.gain_out != nullptr) reinterpret_cast<TA*>(p.aout)[(size_t)b * p.ldao + n0 + lane] = from_f<TA>(xn * gn);
+        const float sq = wave_sum(xn * xn);
+        if (lane == 0 && p.ss_out != nullptr) p.ss_out[(size_t)blockIdx.x * p.B + b] = sq;
+      }
+      if (tid == 0) __hip_atomic_store(p.counters + blockIdx.x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -260,22 +375,24 @@ __global__ void gemv_reduce(GemvArgs p, int splits) {
   }
 }
 
-template <typename TX, typename OT, int NB, int EPI>
+template <typename TA, typename OT, int NB, int EPI, bool NSCALE>
 static hipError_t gemv_launch(const GemvArgs& p, hipStream_t s) {
-  constexpr bool F32X = sizeof(TX) == 4;
+  constexpr bool F32X = sizeof(TA) == 4;
   const int splits = gemv_splits(p.N, p.K, p.B, F32X);
   const int chunks = p.K / GV_KC;
   const int kc = (chunks + splits - 1) / splits * GV_KC;
   dim3 grid(p.N / GV_ROWS, splits);
   if (splits == 1) {
-    hipLaunchKernelGGL((gemv_kernel<TX, OT, NB, EPI, true>), grid, dim3(256), 0, s, p, kc);
+    hipLaunchKernelGGL((gemv_kernel<TA, OT, NB, EPI, true, NSCALE>), grid, dim3(256), 0, s, p, kc);
     return hipGetLastError();
   }
-  if (!p.partial) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((gemv_kernel<TX, OT, NB, EPI, false>), grid, dim3(256), 0, s, p, kc);
+  if (!p.partial || (EPI == EPI_RESID && p.ss_out != nullptr && p.counters == nullptr)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((gemv_kernel<TA, OT, NB, EPI, false, NSCALE>), grid, dim3(256), 0, s, p, kc);
   hipError_t e = hipGetLastError();
-  // out == null (except for the argmax, whose logits are optional): the caller reduces the partials
+  // out == null (except for the argmax, whose logits are optional): the caller reduces the
+  // partials; a residual producer with tile counters has folded them in already
   if (e != hipSuccess || (p.out == nullptr && EPI != EPI_ARGMAX)) return e;
+  if (EPI == EPI_RESID && p.counters != nullptr) return e;
   const long n = (long)p.B * (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
   hipLaunchKernelGGL((gemv_reduce<OT, EPI>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, splits);
   return hipGetLastError();
@@ -286,9 +403,15 @@ hipError_t gemv(const GemvArgs& p, int epi, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
   if (p.B > 32 || p.N % GV_ROWS || p.K <= 0 || p.K % GV_KC || p.ldx % 8 || p.ldw % 8) return hipErrorInvalidValue;
   if (epi == EPI_ARGMAX && (!p.argmax_keys || p.N % 64)) return hipErrorInvalidValue;
-  const bool two = p.B > 16;
-#define NOVA_GEMV_CASE(E)                                                             \
-  case E: return two ? gemv_launch<TX, OT, 2, E>(p, s) : gemv_launch<TX, OT, 1, E>(p, s);
+  if (p.ss_in != nullptr && (p.ss_parts <= 0 || p.ss_parts > 64)) return hipErrorInvalidValue;
+  if ((p.ss_out != nullptr || p.counters != nullptr || p.gain_out != nullptr) && (epi != EPI_RESID || p.out == nullptr))
+    return hipErrorInvalidValue;
+  if (p.gain_out != nullptr && p.aout == nullptr) return hipErrorInvalidValue;
+  const bool two = p.B > 16, norm = p.ss_in != nullptr;
+#define NOVA_GEMV_CASE(E)                                                                                 \
+  case E:                                                                                                 \
+    if (norm) return two ? gemv_launch<TX, OT, 2, E, true>(p, s) : gemv_launch<TX, OT, 1, E, true>(p, s); \
+    return two ? gemv_launch<TX, OT, 2, E, false>(p, s) : gemv_launch<TX, OT, 1, E, false>(p, s);
   switch (epi) {
     NOVA_GEMV_CASE(EPI_STORE)
     NOVA_GEMV_CASE(EPI_RESID)

@@ -329,6 +329,51 @@ hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ decode step start
+// One workgroup per sequence: gather the token's embedding row into the fp32 residual stream,
+// write it times the first RMSNorm's gain for the first projection, and sum its squares (the
+// norm's statistic, as part 0 of its per-tile parts); clear the argmax keys and tile counters.
+template <typename T>
+__global__ void __launch_bounds__(256) decode_embed_kernel(const int* __restrict__ ids, const bf16_t* __restrict__ embed,
+                                                           int H, const bf16_t* __restrict__ g, float* __restrict__ x,
+                                                           T* __restrict__ a, float* __restrict__ ss0, int ss_parts,
+                                                           unsigned long long* __restrict__ keys,
+                                                           unsigned* __restrict__ counters, int n_counters) {
+  __shared__ float red[4];
+  const int b = blockIdx.x, B = gridDim.x;
+  const bf16_t* e = embed + (size_t)ids[b] * H;
+  float* xr = x + (size_t)b * H;
+  T* ar = a + (size_t)b * H;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < H; c += 256) {
+    const float v = bf2f(e[c]);
+    xr[c] = v;
+    ar[c] = from_f<T>(v * bf2f(g[c]));
+    ss += v * v;
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  for (int t = 1 + threadIdx.x; t < ss_parts; t += 256) ss0[(size_t)t * B + b] = 0.f;
+  if (threadIdx.x == 0) keys[b] = 0ull;
+  if (b == 0)
+    for (int i = threadIdx.x; i < n_counters; i += 256) counters[i] = 0u;
+  __syncthreads();
+  if (threadIdx.x == 0) ss0[b] = red[0] + red[1] + red[2] + red[3];
+}
+
+template <typename T>
+hipError_t decode_embed(const int* ids, int B, const bf16_t* embed, int H, const bf16_t* g, float* x, T* a, float* ss0,
+                        int ss_parts, unsigned long long* keys, unsigned* counters, int n_counters, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL((decode_embed_kernel<T>), dim3(B), dim3(256), 0, s, ids, embed, H, g, x, a, ss0, ss_parts, keys,
+                     counters, n_counters);
+  return hipGetLastError();
+}
+template hipError_t decode_embed<bf16_t>(const int*, int, const bf16_t*, int, const bf16_t*, float*, bf16_t*, float*, int,
+                                         unsigned long long*, unsigned*, int, hipStream_t);
+template hipError_t decode_embed<float>(const int*, int, const bf16_t*, int, const bf16_t*, float*, float*, float*, int,
+                                        unsigned long long*, unsigned*, int, hipStream_t);
+
 // ------------------------------------------------------------------ CU placement probe
 __global__ void cu_probe_kernel(uint32_t* __restrict__ out, int n) {
   if (threadIdx.x == 0 && (int)blockIdx.x < n) {

@@ -40,6 +40,23 @@ struct GemvArgs {
   void* out; int ldo;
   float* partial;
   unsigned long long* argmax_keys;
+  // RMSNorm folded into its neighbours.  Consumer: when ss_in is set, X holds x * gain (the
+  // residual times the norm's gain, written by the producer) and output column b is scaled by
+  // rsqrt(sum_t ss_in[t * B + b] / K + eps) over t < ss_parts, the per-tile partial sums of
+  // squares of row b of x (added in a fixed order, so results do not depend on scheduling).
+  const float* ss_in = nullptr;
+  int ss_parts = 0;
+  float eps = 0.f;
+  // Residual producer (EPI_RESID into fp32 out): ss_out[t * B + b] receives the sum of squares of
+  // the updated row b over output tile t (64 rows of N), and when gain_out is set aout[b][n] =
+  // x_new[b][n] * gain_out[n] in the activation type (row pitch ldao).  With split-K,
+  // counters[N / 64] (zero on entry, zero again on exit) let the last split of each tile fold all
+  // partials into out.
+  float* ss_out = nullptr;
+  unsigned* counters = nullptr;
+  const bf16_t* gain_out = nullptr;
+  void* aout = nullptr;
+  int ldao = 0;
 };
 int gemv_splits(int N, int K, int B, bool f32x);
 size_t gemv_partial_floats(int B, int N, int K, bool f32x);
@@ -107,6 +124,12 @@ hipError_t resid_rmsnorm(const float* partial, int splits, float* x, int B, int 
 // ids[b] = the token id packed in keys[b] by the fused argmax.
 hipError_t argmax_finish(const unsigned long long* keys, int B, int* ids, hipStream_t s);
 // x[r] = r < n_vis ? vis[r] : embed[ids[r - n_vis]]  (fp32 out)
+// Decode step start: x[b] = embed[ids[b]] (fp32), a[b] = x[b] * g in the activation type;
+// ss0[0 * B + b] = sum of squares of x[b] and ss0[t * B + b] = 0 for 0 < t < ss_parts; zeroes
+// keys[B] and counters[n_counters].
+template <typename T>
+hipError_t decode_embed(const int* ids, int B, const bf16_t* embed, int H, const bf16_t* g, float* x, T* a, float* ss0,
+                        int ss_parts, unsigned long long* keys, unsigned* counters, int n_counters, hipStream_t s);
 template <typename T>
 hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const bf16_t* embed, int H, float* x,
                       hipStream_t s);

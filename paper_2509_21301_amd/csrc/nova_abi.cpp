@@ -523,29 +523,49 @@ size_t prefill_ws(const nova_llm* m, int S, Carve* cv) {
   return w.used;
 }
 template <typename T>
-size_t decode_ws(const nova_llm* m, int B, int max_ctx, Carve* cv) {
+struct DecodeBufs {
+  float* x;                   // residual stream [B][H]
+  T* a;                       // x times the next RMSNorm's gain, input of the next projection [B][H]
+  float* qkv;                 // QKV projection (fp32) when not split
+  T* q;                       // rotated queries
+  T* att;                     // attention output
+  T* hm;                      // MLP hidden
+  unsigned long long* keys;   // greedy argmax keys
+  float* ss;                  // per-tile row sums of squares of the 2 L + 1 fused RMSNorms [2L+1][H/64][B]
+  unsigned* counters;         // split-K arrival counters of the O and down projections [2L][H/64]
+  float* part;                // split-K partials
+  float* apart;               // decode-attention split partials
+  size_t used;
+};
+
+// The decode step's workspace, carved from base (sizes only when base is null).
+template <typename T>
+DecodeBufs<T> decode_bufs(const nova_llm* m, int B, int max_ctx, void* base) {
   const nova_llm_config& c = m->d.cfg;
-  Carve tmp(nullptr);
-  Carve& w = cv ? *cv : tmp;
+  Carve w(base);
+  DecodeBufs<T> d;
   const size_t H = c.hidden;
-  w.take<float>((size_t)B * H);                         // residual
-  w.take<T>((size_t)B * H);                             // normed
-  w.take<float>((size_t)B * m->qkvw);                   // qkv (fp32 from the thin GEMM)
-  w.take<T>((size_t)B * c.n_q * c.head_dim);            // rotated q
-  w.take<T>((size_t)B * c.n_q * c.head_dim);            // attention out
-  w.take<T>((size_t)B * m->ip);                         // MLP hidden
-  w.take<unsigned long long>((size_t)B);                // argmax keys
-  size_t part = 0;
   const int qd = c.n_q * c.head_dim;
+  d.x = w.take<float>((size_t)B * H);
+  d.a = w.take<T>((size_t)B * H);
+  d.qkv = w.take<float>((size_t)B * m->qkvw);
+  d.q = w.take<T>((size_t)B * qd);
+  d.att = w.take<T>((size_t)B * qd);
+  d.hm = w.take<T>((size_t)B * m->ip);
+  d.keys = w.take<unsigned long long>((size_t)B);
+  d.ss = w.take<float>((size_t)(2 * c.layers + 1) * (H / 64) * B);
+  d.counters = w.take<unsigned>((size_t)2 * c.layers * (H / 64));
+  size_t part = 0;
   const bool f32 = sizeof(T) == 4;
   part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden, f32));
   part = std::max(part, nova::gemv_partial_floats(B, c.hidden, qd, f32));
   part = std::max(part, nova::gemv_partial_floats(B, 2 * m->ip, c.hidden, f32));
   part = std::max(part, nova::gemv_partial_floats(B, c.hidden, m->ip, f32));
   part = std::max(part, nova::gemv_partial_floats(B, c.vocab, c.hidden, f32));
-  w.take<float>(part);
-  w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, c.head_dim, max_ctx, c.n_kv));
-  return w.used;
+  d.part = w.take<float>(part);
+  d.apart = w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, c.head_dim, max_ctx, c.n_kv));
+  d.used = w.used;
+  return d;
 }
 }  // namespace
 
@@ -555,8 +575,8 @@ extern "C" size_t nova_llm_prefill_workspace_bytes(const nova_llm* m, int seq) {
 }
 extern "C" size_t nova_llm_decode_workspace_bytes(const nova_llm* m, int batch, int max_ctx) {
   if (!m || batch <= 0 || max_ctx <= 0) return 0;
-  return m->d.cfg.act == NOVA_ACT_F32 ? decode_ws<float>(m, batch, max_ctx, nullptr)
-                                      : decode_ws<bf16_t>(m, batch, max_ctx, nullptr);
+  return m->d.cfg.act == NOVA_ACT_F32 ? decode_bufs<float>(m, batch, max_ctx, nullptr).used
+                                      : decode_bufs<bf16_t>(m, batch, max_ctx, nullptr).used;
 }
 
 namespace {
@@ -622,77 +642,102 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
                  const nova_kv* kv, int* next_ids, float* logits_out, void* ws, hipStream_t s) {
   const nova_llm_config& c = m->d.cfg;
   const int H = c.hidden, D = c.head_dim, qd = c.n_q * D;
-  Carve w(ws);
-  float* x = w.take<float>((size_t)B * H);
-  T* a = w.take<T>((size_t)B * H);
-  float* qkv = w.take<float>((size_t)B * m->qkvw);
-  T* q = w.take<T>((size_t)B * qd);
-  T* att = w.take<T>((size_t)B * qd);
-  T* hm = w.take<T>((size_t)B * m->ip);
-  unsigned long long* keys = w.take<unsigned long long>((size_t)B);
-  const bool f32 = sizeof(T) == 4;
-  size_t partn = 0;
-  partn = std::max(partn, nova::gemv_partial_floats(B, m->qkvw, H, f32));
-  partn = std::max(partn, nova::gemv_partial_floats(B, H, qd, f32));
-  partn = std::max(partn, nova::gemv_partial_floats(B, 2 * m->ip, H, f32));
-  partn = std::max(partn, nova::gemv_partial_floats(B, H, m->ip, f32));
-  partn = std::max(partn, nova::gemv_partial_floats(B, c.vocab, H, f32));
-  float* part = w.take<float>(partn);
-  float* apart = w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, D, max_ctx, c.n_kv));
+  const DecodeBufs<T> d = decode_bufs<T>(m, B, max_ctx, ws);
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
-
-  // Split-K projections leave their partials for the next kernel: the QKV partials are summed by
-  // the rotary/KV-append kernel, the O and down partials by the fused residual + RMSNorm.
+  const bool f32 = sizeof(T) == 4;
+  const int tiles = H / 64;
   const int sp_qkv = nova::gemv_splits(m->qkvw, H, B, f32);
-  const int sp_o = nova::gemv_splits(H, qd, B, f32);
-  const int sp_down = nova::gemv_splits(H, m->ip, B, f32);
   const char* hw = (const char*)m->d.head;
   auto layer_w = [&](int l, int i) {
     return (const bf16_t*)((const char*)m->d.layers + (size_t)l * m->lay.bytes + m->lay.off[i]);
   };
-  CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(nullptr, 0, ids, B, (const bf16_t*)m->d.embed, H, x, s));
-  if (c.layers > 0)
-    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, x, B, H, layer_w(0, 0), c.eps, a, H, nullptr, s));
-  else
-    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, x, B, H, (const bf16_t*)(hw + m->head.off[0]), c.eps, a, H,
-                                                   keys, s));
-  for (int l = 0; l < c.layers; ++l) {
-    auto W = [&](int i) { return layer_w(l, i); };
-    const bf16_t* next_gain = l + 1 < c.layers ? layer_w(l + 1, 0) : (const bf16_t*)(hw + m->head.off[0]);
+  const bf16_t* final_gain = (const bf16_t*)(hw + m->head.off[0]);
+  auto attention_block = [&](int l) -> int {
     T* kp = (T*)kv->k + l * kv_layer;
     T* vp = (T*)kv->v + l * kv_layer;
-    {
-      GemvArgs p{a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : qkv, m->qkvw, part, nullptr};
-      CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
+    CALL(NOVA_KIND_MISC, s, nova::qkv_decode<T>(sp_qkv > 1 ? d.part : d.qkv, sp_qkv, B, c.n_q, c.n_kv, D, c.rope_theta, pos,
+                                                 d.q, kp, vp, tables, max_blocks, c.block, s));
+    nova::DecAttnArgs p{d.q, kp, vp, tables, max_blocks, pos, d.att, d.apart, B, c.n_q, c.n_kv, c.block, max_ctx};
+    CALL(NOVA_KIND_DECODE_ATTN, s, nova::decode_attention<T>(p, D, s));
+    return (int)NOVA_OK;
+  };
+
+  if (B <= 8) {
+    // Small batches: each RMSNorm is folded into its neighbours.  The producer of the residual
+    // (embedding, O and down projections) writes x times the norm's gain and per-tile sums of
+    // squares of x, and the consumer projection (QKV, gate/up, LM head) scales each output by the
+    // row's rsqrt.  (With larger batches the split-K tail of the producers outgrows a separate
+    // norm kernel.)  The QKV split-K partials are summed by the rotary/KV-append kernel.
+    auto ss = [&](int k) { return d.ss + (size_t)k * tiles * B; };
+    CALL(NOVA_KIND_MISC, s, nova::decode_embed<T>(ids, B, (const bf16_t*)m->d.embed, H,
+                                                  c.layers > 0 ? layer_w(0, 0) : final_gain, d.x, d.a, ss(0), tiles, d.keys,
+                                                  d.counters, 2 * c.layers * tiles, s));
+    for (int l = 0; l < c.layers; ++l) {
+      auto W = [&](int i) { return layer_w(l, i); };
+      {
+        GemvArgs p{d.a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : d.qkv, m->qkvw, d.part, nullptr};
+        p.ss_in = ss(2 * l), p.ss_parts = tiles, p.eps = c.eps;
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
+      }
+      if (const int rc = attention_block(l)) return rc;
+      {
+        GemvArgs p{d.att, qd, W(2), qd, B, H, qd, d.x, H, d.part, nullptr};
+        p.ss_out = ss(2 * l + 1), p.counters = d.counters + (size_t)(2 * l) * tiles;
+        p.gain_out = W(3), p.aout = d.a, p.ldao = H;
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
+      }
+      {
+        GemvArgs p{d.a, H, W(4), H, B, 2 * m->ip, H, d.hm, m->ip, d.part, nullptr};
+        p.ss_in = ss(2 * l + 1), p.ss_parts = tiles, p.eps = c.eps;
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
+      }
+      {
+        GemvArgs p{d.hm, m->ip, W(5), m->ip, B, H, m->ip, d.x, H, d.part, nullptr};
+        p.ss_out = ss(2 * l + 2), p.counters = d.counters + (size_t)(2 * l + 1) * tiles;
+        p.gain_out = l + 1 < c.layers ? layer_w(l + 1, 0) : final_gain, p.aout = d.a, p.ldao = H;
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
+      }
     }
-    CALL(NOVA_KIND_MISC, s, nova::qkv_decode<T>(sp_qkv > 1 ? part : qkv, sp_qkv, B, c.n_q, c.n_kv, D, c.rope_theta, pos, q,
-                                                 kp, vp, tables, max_blocks, c.block, s));
-    {
-      nova::DecAttnArgs p{q, kp, vp, tables, max_blocks, pos, att, apart, B, c.n_q, c.n_kv, c.block, max_ctx};
-      CALL(NOVA_KIND_DECODE_ATTN, s, nova::decode_attention<T>(p, D, s));
+    GemvArgs p{d.a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, d.part, d.keys};
+    p.ss_in = ss(2 * c.layers), p.ss_parts = tiles, p.eps = c.eps;
+    CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
+  } else {
+    // Larger batches: a residual + RMSNorm kernel sums the O / down split-K partials into x and
+    // writes the normalised rows for the next projection.
+    const int sp_o = nova::gemv_splits(H, qd, B, f32);
+    const int sp_down = nova::gemv_splits(H, m->ip, B, f32);
+    CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(nullptr, 0, ids, B, (const bf16_t*)m->d.embed, H, d.x, s));
+    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, d.x, B, H, c.layers > 0 ? layer_w(0, 0) : final_gain, c.eps,
+                                                   d.a, H, c.layers > 0 ? nullptr : d.keys, s));
+    for (int l = 0; l < c.layers; ++l) {
+      auto W = [&](int i) { return layer_w(l, i); };
+      {
+        GemvArgs p{d.a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : d.qkv, m->qkvw, d.part, nullptr};
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
+      }
+      if (const int rc = attention_block(l)) return rc;
+      {
+        GemvArgs p{d.att, qd, W(2), qd, B, H, qd, sp_o > 1 ? nullptr : d.x, H, d.part, nullptr};
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
+      }
+      CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_o > 1 ? d.part : nullptr, sp_o > 1 ? sp_o : 0, d.x, B, H, W(3), c.eps,
+                                                     d.a, H, nullptr, s));
+      {
+        GemvArgs p{d.a, H, W(4), H, B, 2 * m->ip, H, d.hm, m->ip, d.part, nullptr};
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
+      }
+      {
+        GemvArgs p{d.hm, m->ip, W(5), m->ip, B, H, m->ip, sp_down > 1 ? nullptr : d.x, H, d.part, nullptr};
+        CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
+      }
+      CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_down > 1 ? d.part : nullptr, sp_down > 1 ? sp_down : 0, d.x, B, H,
+                                                     l + 1 < c.layers ? layer_w(l + 1, 0) : final_gain, c.eps, d.a, H,
+                                                     l + 1 < c.layers ? nullptr : d.keys, s));
     }
-    {
-      GemvArgs p{att, qd, W(2), qd, B, H, qd, sp_o > 1 ? nullptr : x, H, part, nullptr};
-      CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
-    }
-    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_o > 1 ? part : nullptr, sp_o > 1 ? sp_o : 0, x, B, H, W(3), c.eps, a, H,
-                                                   nullptr, s));
-    {
-      GemvArgs p{a, H, W(4), H, B, 2 * m->ip, H, hm, m->ip, part, nullptr};
-      CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
-    }
-    {
-      GemvArgs p{hm, m->ip, W(5), m->ip, B, H, m->ip, sp_down > 1 ? nullptr : x, H, part, nullptr};
-      CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
-    }
-    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_down > 1 ? part : nullptr, sp_down > 1 ? sp_down : 0, x, B, H,
-                                                   next_gain, c.eps, a, H, l + 1 < c.layers ? nullptr : keys, s));
-  }
-  {
-    GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, part, keys};
+    GemvArgs p{d.a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, d.part, d.keys};
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
-  CALL(NOVA_KIND_MISC, s, nova::argmax_finish(keys, B, next_ids, s));
+  CALL(NOVA_KIND_MISC, s, nova::argmax_finish(d.keys, B, next_ids, s));
   return NOVA_OK;
 }
 }  // namespace

@@ -5,8 +5,10 @@ one by one (through the C ABI, bf16, tolerance 2e-2):
   (5184 patches each) with the 2x2 merge to 3584 -- sampled merged tokens of both images;
 * prefill: one 3584-wide GQA layer (28/4 heads of 128, SwiGLU 18944, vocab 152064) over
   1300 visual embeddings + 200 text tokens -- last-row logits, greedy id, sampled K/V;
-* decode: 20 sequences with ragged contexts of 1200..1500 tokens in a shuffled paged cache
-  (random bf16 K/V shared with the oracle) -- logits of every sequence and the appended K/V.
+* decode: 4 and 20 sequences with ragged contexts of 1200..1500 tokens in a shuffled paged cache
+  (random bf16 K/V shared with the oracle) -- logits of every sequence and the appended K/V; the
+  small batch runs the step with its RMSNorms folded into the projections, the large one with
+  separate residual + norm kernels.
 """
 import dataclasses
 
@@ -74,12 +76,12 @@ def test_prefill_layer_real_width(gpu_lib, llm1):
         assert vlm.max_rel_err(v5[0, blk, :, :, slot], v[p]) < sc.TOL_BF16
 
 
-def test_decode_batch20_real_width(gpu_lib, llm1):
+@pytest.mark.parametrize("bsz", [4, 20])
+def test_decode_real_width(gpu_lib, llm1, bsz):
     import torch
     nova = gpu_lib
     w, llm = llm1
     cfg = LLM1
-    bsz = 20
     ctx = [1500 - 15 * b for b in range(bsz)]                    # positions of the new tokens
     tables, pool = synth.block_tables([c + 1 for c in ctx], cfg.block, seed=9)
     rng = np.random.default_rng(3)
