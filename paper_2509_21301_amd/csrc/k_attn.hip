@@ -37,8 +37,25 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, lq = lane & 31;
   const int nqb = (p.sq + AQ - 1) / AQ;
-  const int qb = CAUSAL ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;   // heavy causal blocks first
-  const int h = blockIdx.y, b = blockIdx.z;
+  // one-dimensional grid: workgroups are dealt to the 8 XCDs round-robin, so when the (batch,
+  // head) pairs split evenly over the XCDs each XCD takes whole pairs, one after another, and the
+  // pair's K and V stay in its L2 while all of the pair's query blocks read them
+  int qbi, h, b;
+  {
+    const int pairs = p.batch * p.n_q, lin = blockIdx.x;
+    int pair;
+    if (pairs % 8 == 0) {
+      const int j = lin >> 3;
+      pair = (lin & 7) * (pairs >> 3) + j / nqb;
+      qbi = j % nqb;
+    } else {
+      pair = lin / nqb;
+      qbi = lin % nqb;
+    }
+    h = pair % p.n_q;
+    b = pair / p.n_q;
+  }
+  const int qb = CAUSAL ? (nqb - 1 - qbi) : qbi;   // heavy causal blocks first
   const int kvh = h / (p.n_q / p.n_kv);
   const int q0 = qb * AQ;
   const int qrow = q0 + wave * 32 + lq;
@@ -261,7 +278,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
 
 template <typename T, int D>
 static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
-  dim3 grid((p.sq + AQ - 1) / AQ, p.n_q, p.batch);
+  dim3 grid((p.sq + AQ - 1) / AQ * p.n_q * p.batch);
   if (p.causal) hipLaunchKernelGGL((attn_kernel<T, D, true>), grid, dim3(256), 0, s, p);
   else hipLaunchKernelGGL((attn_kernel<T, D, false>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
