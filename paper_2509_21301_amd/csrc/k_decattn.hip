@@ -107,6 +107,21 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
         }
       }
     }
+    // V^T fragments of both blocks, loaded now so that their latency overlaps the softmax: row
+    // d = 16i + col, tokens 4grp..+3 of each block (zero past the table)
+    uint2 vraw[ND][2];
+    float4 vraw32[F32 ? ND : 1][2];
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const T* src = vpool + ((size_t)max(phys[j], 0) * p.n_kv + kvh) * D * DA_BLOCK + (size_t)(16 * i + col) * DA_BLOCK + 4 * grp;
+        if constexpr (F32) {
+          vraw32[i][j] = phys[j] >= 0 ? *reinterpret_cast<const float4*>(src) : float4{0.f, 0.f, 0.f, 0.f};
+        } else {
+          vraw[i][j] = phys[j] >= 0 ? *reinterpret_cast<const uint2*>(src) : make_uint2(0u, 0u);
+        }
+      }
     // lane holds S[token 4*grp + r][head col] for block j; mask tokens beyond the context
     float tmax = -1e30f;
 #pragma unroll
@@ -150,17 +165,10 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
       Frag8 va, vl;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        if (phys[j] >= 0) {
-          const T* src = vpool + ((size_t)phys[j] * p.n_kv + kvh) * D * DA_BLOCK + (size_t)(16 * i + col) * DA_BLOCK + 4 * grp;
-          if constexpr (F32) {
-            *reinterpret_cast<float4*>(vx + 4 * j) = *reinterpret_cast<const float4*>(src);
-          } else {
-            const uint2 t = *reinterpret_cast<const uint2*>(src);
-            va.w[2 * j] = t.x; va.w[2 * j + 1] = t.y;
-          }
+        if constexpr (F32) {
+          *reinterpret_cast<float4*>(vx + 4 * j) = vraw32[i][j];
         } else {
-          if constexpr (F32) { vx[4 * j] = vx[4 * j + 1] = vx[4 * j + 2] = vx[4 * j + 3] = 0.f; }
-          else { va.w[2 * j] = 0u; va.w[2 * j + 1] = 0u; }
+          va.w[2 * j] = vraw[i][j].x; va.w[2 * j + 1] = vraw[i][j].y;
         }
       }
       if constexpr (F32) {
