@@ -224,6 +224,63 @@ class ServingSetup:
         return srv.run(trace)
 
 
+# ----------------------------------------------------------------------------- offload (Sec. 3.5)
+def measure_offload(nova, torch, st, srv, slots=(2, 3, 4)):
+    """The encoder with its 32 layers in pinned host memory, streamed through K device slots (Eq. 7),
+    against the resident encoder, on three encode workloads; plus the Eq. 8 bandwidth each would need
+    to hide the copies, next to the measured pinned host-to-device rate."""
+    lb, L = st.vit.layer_bytes, st.vc.layers
+    host = torch.empty(st.vit.layers.numel(), dtype=torch.bfloat16, pin_memory=True)
+    host.copy_(st.vit.layers)
+    dev = torch.empty_like(st.vit.layers)
+    stream = torch.cuda.current_stream()
+    dev.copy_(host, non_blocking=True)
+    h2d_ms = time_passes(torch, lambda: dev.copy_(host, non_blocking=True), 3, stream)
+    del dev
+    h2d_gbs = host.numel() * 2 / (h2d_ms / 1e3) / 1e9
+    work = [("screenshot_1092x2408_b1", srv.vit, srv.pixels, srv.vis),
+            ("image_1008x1008_b1", st.vit, st.pixels[:1], st.enc_out[:1]),
+            ("image_1008x1008_b8", st.vit, st.pixels, st.enc_out)]
+    def per_pass(fn, warm=2, reps=5):
+        # back-to-back passes (so a pass's head copies overlap the previous pass's tail), one event between
+        # each two; median and best, since a pass now and then runs long on this box, resident ones too
+        for _ in range(warm):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(stream)
+        for i in range(reps):
+            fn()
+            ev[i + 1].record(stream)
+        ev[-1].synchronize()
+        ts = sorted(a.elapsed_time(b) for a, b in zip(ev, ev[1:]))
+        return ts[len(ts) // 2], ts[0]
+
+    rows = []
+    for name, vit, px, out in work:
+        t_res, t_res_min = per_pass(lambda: vit.encode(px, out=out))
+        ref = out.clone()
+        # Eq. 8: hiding every copy needs B >= (S / T) (L - K) / (L - 2), S the whole encoder's bytes
+        row = {"workload": name, "resident_ms": round(t_res, 3), "resident_best_ms": round(t_res_min, 3),
+               "resident_layer_mb": round(L * lb / 1e6, 1)}
+        for K in slots:
+            ov = nova.Vit(vit.cfg, None, blobs=(vit.embed, host, vit.head, lb), n_slots=K)
+            t_off, t_off_min = per_pass(lambda: ov.encode(px, out=out))
+            same = bool(torch.equal(out, ref))
+            need = (L * lb) / (t_res / 1e3) * (L - K) / (L - 2) / 1e9
+            row[f"k{K}"] = {"ms": round(t_off, 3), "best_ms": round(t_off_min, 3),
+                            "overhead_pct": round(100 * (t_off / t_res - 1), 1),
+                            "slot_mb": round(K * lb / 1e6, 1), "eq8_needed_gbs": round(need, 1),
+                            "bit_identical": same}
+            torch.cuda.synchronize()
+            del ov
+        rows.append(row)
+        log(f"offload {name}: resident {t_res:.2f} ms; " + ", ".join(
+            f"K={K} {row[f'k{K}']['ms']:.2f} ms (+{row[f'k{K}']['overhead_pct']}%, Eq. 8 needs "
+            f"{row[f'k{K}']['eq8_needed_gbs']} GB/s)" for K in slots))
+    del host
+    return {"h2d_pinned_gbs": round(h2d_gbs, 1), "layer_mb": round(lb / 1e6, 2), "layers": L, "runs": rows}
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 def cpu_baseline(synth):
     """The oracle, as is, on one image's worth of encoder layers at the real shape (2 of 32
@@ -269,9 +326,10 @@ def main():
     ap.add_argument("--rates", type=float, nargs="+", default=[2.0, 4.0], help="request rates (req/s) of the serving runs")
     ap.add_argument("--window", type=float, default=10.0, help="arrival window (s) of each serving run")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
-    ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32", "copy"],
+    ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32", "copy", "offload"],
                     help="run only this stage in a loop of --steps passes (for rocprofv3); 'copy' is a plain "
-                         "1 GiB device copy that calibrates the HBM byte counters")
+                         "1 GiB device copy that calibrates the HBM byte counters; 'offload' runs only the "
+                         "layer-offload comparison")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the method serves all three stages on a single GPU; "
@@ -295,6 +353,9 @@ def main():
     B = args.batch
     stream = torch.cuda.current_stream()
 
+    if args.profile_stage == "offload":
+        print(json.dumps(measure_offload(nova, torch, st, ServingSetup(nova, torch, synth, st))), flush=True)
+        return
     if args.profile_stage:
         fn = st.prefill if args.profile_stage == "prefill" else (lambda: st.decode(int(args.profile_stage[6:])))
         for _ in range(args.warmup):
@@ -430,6 +491,8 @@ def main():
                 log(f"co-run decode {p} / {other} {256 - p}: {other} {t_oc:.2f} ms (solo {t_o:.2f}), "
                     f"decode step {t_dc:.3f} ms (solo {t_d:.3f})")
         result["corun"] = corun
+        # offload: the Sec. 3.5 ring against the resident encoder, with the Eq. 8 bandwidth check
+        result["offload"] = measure_offload(nova, torch, st, srv)
         curves = sched.StageCurves.from_corun(corun)
         out_len = 32.0                                   # mean of the U{16..48} output lengths
         pv, pp, lat = sched.best_static(curves, out_len)

@@ -109,16 +109,26 @@ size_t nova_vit_workspace_bytes(const nova_vit* vit, int batch);
 /* Vision encode of `batch` images.
  *  pixels: device bf16 [batch, image_h, image_w, 3] (HWC, values fed as is)
  *  out:    device act-type [batch, n_patches / merge^2, out_hidden]
- * With offload, every layer waits for its slot's copy and, once done, swaps in layer
- * (l + K) mod L (Eq. 7), so the next call's first K layers are loaded during this one. */
+ * With offload, every layer waits for its slot's copy and, once done, its slot receives layer
+ * (l + K) mod L (Eq. 7), so the next call's first K layers are loaded during this one.  When K
+ * does not divide L the layer-to-slot map rotates from one call to the next. */
 int nova_vit_encode(nova_vit* vit, const void* pixels, int batch, void* out, void* ws, size_t ws_bytes,
                     nova_stream_t stream);
 
-/* Swap logical ViT layer `layer` into slot layer % K from pinned host memory on copy_stream
+/* Swap logical ViT layer `layer` into a physical slot from pinned host memory on copy_stream
  * (0: the model's own copy stream), after the last compute use of that slot has finished
- * (Sec. 3.5: one event per physical layer guards both the copy and the compute).  Use it to
- * preload layers 0..K-1 before the first encode.  Returns NOVA_EINVAL without offload. */
+ * (Sec. 3.5: one event per physical layer guards both the copy and the compute).  No-op if the
+ * layer is already in a slot.  The slot is the one holding layer (layer - K) mod L (the Eq. 7
+ * ring), else an empty one, else slot layer mod K.  nova_vit_encode queues layers 0..K-1 this
+ * way itself; calling it earlier moves those copies ahead of the first encode.  Returns
+ * NOVA_EINVAL without offload. */
 int nova_prefetch_layer(nova_vit* vit, int layer, nova_stream_t copy_stream);
+
+/* Offload ring state, host side: slot_layer (may be NULL) receives the n_slots logical layers
+ * the physical slots hold or are receiving (-1: none yet), copies (may be NULL) the number of
+ * host-to-device layer copies issued since creation.  Over repeated encodes the ring issues L
+ * copies per call (Eq. 7).  Returns NOVA_EINVAL without offload. */
+int nova_vit_offload_state(const nova_vit* vit, int* slot_layer, unsigned long long* copies);
 
 /* ------------------------------------------------------------------ LLM (Sec. 2.1, Sec. 3.4)
  * Decoder layer: RMSNorm -> q, k, v (no bias) -> rotary embedding (half-split pairs) -> causal

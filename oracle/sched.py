@@ -69,6 +69,18 @@ def next_layer(cur, k, n_layers):
     return (cur + k) % n_layers
 
 
+def ring_slots(n_layers, k, passes):
+    """Sec. 3.5 stepped pass by pass: physical slots start with logical layers 0..K-1; when a
+    layer's forward finishes, its slot takes the Eq. 7 successor.  Returns the layer each slot
+    holds after ``passes`` full forward passes."""
+    slots = list(range(k))
+    for _ in range(passes):
+        for layer in range(n_layers):
+            slot = slots.index(layer)
+            slots[slot] = next_layer(layer, k, n_layers)
+    return slots
+
+
 def offload_ok(size, t_fwd, bandwidth, n_layers, k):
     """Eq. 8 stated per layer: for every l in [K+1, L] the copy of (l-K)/L of the weights
     (size S at bandwidth B) must fit in the (l-2)/L of the forward time T before layer l."""

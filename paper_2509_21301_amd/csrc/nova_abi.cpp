@@ -279,9 +279,31 @@ struct nova_vit {
   bool offload = false;
   hipStream_t copy_stream = nullptr;
   std::vector<hipEvent_t> ready, freed;
-  std::vector<int> slot_layer;
+  std::vector<int> slot_layer;            // logical layer each physical slot holds (or is receiving), -1 if none
   std::vector<char> freed_recorded;
+  unsigned long long copies = 0;          // host-to-device layer copies issued so far
 };
+
+namespace {
+int find_slot(const nova_vit* v, int layer) {
+  for (int p = 0; p < (int)v->slot_layer.size(); ++p)
+    if (v->slot_layer[p] == layer) return p;
+  return -1;
+}
+
+// Copy logical layer `layer` into physical slot p on stream cs, once the last compute use of p
+// has finished; the slot's ready event then marks the copy done.
+int copy_into_slot(nova_vit* v, int layer, int p, hipStream_t cs) {
+  if (v->freed_recorded[p]) HIP_TRY(hipStreamWaitEvent(cs, v->freed[p], 0));
+  const size_t lb = v->lay.bytes;
+  HIP_TRY(hipMemcpyAsync((char*)v->d.slots + (size_t)p * lb, (const char*)v->d.host_layers + (size_t)layer * lb, lb,
+                         hipMemcpyHostToDevice, cs));
+  HIP_TRY(hipEventRecord(v->ready[p], cs));
+  v->slot_layer[p] = layer;
+  ++v->copies;
+  return NOVA_OK;
+}
+}  // namespace
 
 extern "C" int nova_vit_create(const nova_vit_desc* desc, nova_vit** out) {
   if (!desc || !out) return fail(NOVA_EINVAL, "null argument");
@@ -365,14 +387,21 @@ extern "C" int nova_prefetch_layer(nova_vit* v, int layer, nova_stream_t cs_in) 
   if (!v->offload) return fail(NOVA_EINVAL, "model has no layer offload");
   if (layer < 0 || layer >= v->d.cfg.layers) return fail(NOVA_EINVAL, "layer %d out of range", layer);
   hipStream_t cs = cs_in ? (hipStream_t)cs_in : v->copy_stream;
-  const int K = v->d.n_slots, slot = layer % K;
-  if (v->slot_layer[slot] == layer) return NOVA_OK;     // already resident (or in flight)
-  if (v->freed_recorded[slot]) HIP_TRY(hipStreamWaitEvent(cs, v->freed[slot], 0));
-  const size_t lb = v->lay.bytes;
-  HIP_TRY(hipMemcpyAsync((char*)v->d.slots + (size_t)slot * lb, (const char*)v->d.host_layers + (size_t)layer * lb, lb,
-                         hipMemcpyHostToDevice, cs));
-  HIP_TRY(hipEventRecord(v->ready[slot], cs));
-  v->slot_layer[slot] = layer;
+  if (find_slot(v, layer) >= 0) return NOVA_OK;        // already resident (or in flight)
+  // the slot Eq. 7 gives it: the one that holds layer - K; else an empty one; else slot layer mod K
+  const int K = v->d.n_slots, L = v->d.cfg.layers;
+  int p = find_slot(v, ((layer - K) % L + L) % L);
+  if (p < 0) p = find_slot(v, -1);
+  if (p < 0) p = layer % K;
+  return copy_into_slot(v, layer, p, cs);
+}
+
+extern "C" int nova_vit_offload_state(const nova_vit* v, int* slot_layer, unsigned long long* copies) {
+  if (!v) return fail(NOVA_EINVAL, "null vit");
+  if (!v->offload) return fail(NOVA_EINVAL, "model has no layer offload");
+  if (slot_layer)
+    for (int p = 0; p < v->d.n_slots; ++p) slot_layer[p] = v->slot_layer[p];
+  if (copies) *copies = v->copies;
   return NOVA_OK;
 }
 
@@ -400,13 +429,18 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
     CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_POS, s)));
   }
   const int L = c.layers, K = v->offload ? v->d.n_slots : 0;
+  // the first K layers: already in their slots after an earlier call (its tail loaded them), else
+  // all K copies are queued here at once rather than one per layer
+  for (int l = 0; l < K; ++l)
+    if (int rc = nova_prefetch_layer(v, l, nullptr)) return rc;
   for (int l = 0; l < L; ++l) {
     const char* lw;
+    int slot = -1;
     if (v->offload) {
-      const int slot = l % K;
-      if (v->slot_layer[slot] != l) {
-        int rc = nova_prefetch_layer(v, l, nullptr);
-        if (rc) return rc;
+      slot = find_slot(v, l);
+      if (slot < 0) {
+        if (int rc = nova_prefetch_layer(v, l, nullptr)) return rc;
+        slot = find_slot(v, l);
       }
       HIP_TRY(hipStreamWaitEvent(s, v->ready[slot], 0));
       lw = (const char*)v->d.slots + (size_t)slot * v->lay.bytes;
@@ -439,11 +473,12 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
     }
     if (v->offload) {
-      const int slot = l % K;
+      // Eq. 7: the slot that held layer l receives layer (l + K) mod L once l's kernels are done
       HIP_TRY(hipEventRecord(v->freed[slot], s));
       v->freed_recorded[slot] = 1;
-      int rc = nova_prefetch_layer(v, (l + K) % L, nullptr);   // Eq. 7
-      if (rc) return rc;
+      const int nxt = (l + K) % L;
+      if (find_slot(v, nxt) < 0)
+        if (int rc = copy_into_slot(v, nxt, slot, v->copy_stream)) return rc;
     }
   }
   // adapter: LN per patch scattered into merged rows, then one Linear

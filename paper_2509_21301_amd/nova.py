@@ -68,6 +68,7 @@ _SIG = {
     "nova_vit_workspace_bytes": (C.c_size_t, [C.c_void_p, C.c_int]),
     "nova_vit_encode": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "nova_prefetch_layer": (C.c_int, [C.c_void_p, C.c_int, C.c_void_p]),
+    "nova_vit_offload_state": (C.c_int, [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_ulonglong)]),
     "nova_llm_layer_layout": (C.c_int, [C.POINTER(LlmConfigC), C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
     "nova_llm_head_layout": (C.c_int, [C.POINTER(LlmConfigC), C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
     "nova_llm_create": (C.c_int, [C.POINTER(LlmDescC), C.POINTER(C.c_void_p)]),
@@ -270,6 +271,7 @@ class Vit:
             desc.host_layers = _ptr(self.layers)
             desc.slots = _ptr(self.slots)
             desc.n_slots = n_slots
+            self.slots_n = n_slots
         else:
             desc.layers = _ptr(self.layers)
         h = C.c_void_p()
@@ -299,9 +301,16 @@ class Vit:
     def prefetch(self, layer, stream=None):
         _check(lib.nova_prefetch_layer(self.h, layer, None if stream is None else stream.cuda_stream))
 
+    def offload_state(self):
+        """(logical layer held by each physical slot, layer copies issued so far)."""
+        k = C.c_int * self.slots_n
+        sl, n = k(), C.c_ulonglong()
+        _check(lib.nova_vit_offload_state(self.h, sl, C.byref(n)))
+        return list(sl), n.value
+
     def __del__(self):
         h = getattr(self, "h", None)
-        if h is not None and h.value:
+        if h is not None and h.value and lib is not None:
             lib.nova_vit_destroy(h)
             self.h = None
 
@@ -361,7 +370,7 @@ class Llm:
 
     def __del__(self):
         h = getattr(self, "h", None)
-        if h is not None and h.value:
+        if h is not None and h.value and lib is not None:
             lib.nova_llm_destroy(h)
             self.h = None
 

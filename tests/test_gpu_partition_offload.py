@@ -12,6 +12,7 @@
 import numpy as np
 import pytest
 
+from oracle import sched as osched
 from oracle import vlm
 from paper_2509_21301_amd import synth
 from tests import stage_cases as sc
@@ -140,4 +141,9 @@ def test_offload_bit_identical_to_resident(gpu_lib, vit5, k_slots):
     for call in range(3):            # the ring wraps: each call's tail loads the next call's head
         got = off.encode(px).cpu()
         assert torch.equal(got, resident), f"call {call}"
+        # one copy per layer per call after the K preloads, slots rotating as Eq. 7 says (K = 3
+        # does not divide L = 5)
+        slots, copies = off.offload_state()
+        assert copies == k_slots + (call + 1) * VIT5.layers
+        assert slots == osched.ring_slots(VIT5.layers, k_slots, call + 1)
     torch.cuda.synchronize()

@@ -358,6 +358,20 @@ def test_eq7_worked_example():
     assert sched.next_layer(63, 2, 64) == 1               # wraps into the next pass
 
 
+def test_ring_slots_worked_by_hand():
+    # L = 5, K = 3, one pass: slot 0 holds 0 then 3, and after 3 takes 1; slot 1 holds 1, 4, then 2;
+    # slot 2 holds 2, then 0
+    assert sched.ring_slots(5, 3, 1) == [1, 2, 0]
+    assert sched.ring_slots(5, 3, 2) == [2, 0, 1]
+    # K divides L: every slot keeps its residue class, so the map never moves
+    assert sched.ring_slots(6, 3, 4) == [0, 1, 2]
+    assert sched.ring_slots(64, 2, 3) == [0, 1]
+    # after any number of passes the slots hold the next pass's first K layers
+    for n_layers, k in [(5, 2), (5, 3), (7, 4), (32, 3)]:
+        for passes in range(4):
+            assert sorted(sched.ring_slots(n_layers, k, passes)) == list(range(k))
+
+
 def test_eq8_printed_bound_and_closed_form():
     g = GOLDEN["eq8_bandwidth"]
     need = [sched.offload_min_bandwidth(g["size_gb"], t, g["vit_layers"], 2) for t in g["t_fwd_s"]]
