@@ -75,7 +75,18 @@ NOVA_DEV void rope_sincos(int pos, int c, int D, float theta, float* sn, float* 
   sincosf((float)ang, sn, cs);
 }
 
-NOVA_DEV float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// erf by the rational approximation of Abramowitz & Stegun, formula 7.1.26 (after Hastings):
+// erf(a) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-a^2), t = 1 / (1 + p a), a >= 0,
+// absolute error at most 1.5e-7; odd in x.  One reciprocal and one exp, no branches, which makes
+// the GELU epilogue of the vision MLP several times cheaper than the library erf.
+NOVA_DEV float erf_as(float x) {
+  const float a = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+  const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f),
+                                      -0.284496736f), 0.254829592f);
+  return copysignf(1.0f - poly * __expf(-a * a), x);
+}
+NOVA_DEV float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
 NOVA_DEV float silu(float x) { return x / (1.0f + __expf(-x)); }
 
 // Kernel timing categories (host side).
