@@ -225,7 +225,7 @@ class ServingSetup:
 
 
 # ----------------------------------------------------------------------------- offload (Sec. 3.5)
-def measure_offload(nova, torch, st, srv, slots=(2, 3, 4)):
+def measure_offload(nova, torch, st, srv, slots=(2, 3, 4, 5)):
     """The encoder with its 32 layers in pinned host memory, streamed through K device slots (Eq. 7),
     against the resident encoder, on three encode workloads; plus the Eq. 8 bandwidth each would need
     to hide the copies, next to the measured pinned host-to-device rate."""
@@ -523,7 +523,9 @@ def main():
                             "decode_cus": list(kw.get("decode_cus", (256, 256)))})
                 serving.append(res)
                 log(f"serve {mode:16s} rate {rate}: max E2E {res['max_e2e_s']:.3f} s, avg {res['avg_e2e_s']:.3f} s, "
-                    f"avg TBT {res['avg_tbt_ms']:.1f} ms, {res['throughput_req_s']:.2f} req/s")
+                    f"avg TBT {res['avg_tbt_ms']:.1f} ms, {res['throughput_req_s']:.2f} req/s, decode batch "
+                    f"{res['avg_decode_batch']:.2f}, vision wait {res['avg_queue_wait_s']:.3f} s (Eq. 6: "
+                    f"{res['eq6_predicted_wait_s']})")
         result["serving"] = serving
 
     if not args.no_cpu:

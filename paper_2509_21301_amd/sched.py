@@ -84,6 +84,13 @@ def queue_wait(t_service: float, rate: float) -> float:
     return float("inf") if rho >= 1.0 else rate * t_service * t_service / (2.0 * (1.0 - rho))
 
 
+def mg1_wait(rate: float, mean_t: float, mean_t2: float) -> float:
+    """Eq. 6 with measured moments of the service time T = t_vision + t_prefill:
+    lambda E[T^2] / (2 (1 - lambda E[T])); infinite when the server is saturated."""
+    rho = rate * mean_t
+    return float("inf") if rho >= 1.0 else rate * mean_t2 / (2.0 * (1.0 - rho))
+
+
 def best_under_load(c: StageCurves, out_len: float, rate: float):
     """The partition pair minimising Eq. 1 plus the Eq. 6 queueing delay at `rate` (the Pareto
     point the request rate calls for: fewer decode CUs as the rate grows).  Returns

@@ -99,6 +99,8 @@ class Server:
         self.n_pending = 0            # requests queued for or inside vision encode / prefill
         self.decode_active = 0        # requests in the decode batch or waiting to join it
         self.partition_log = []
+        self.decode_batches = []      # batch size of every decode step
+        self.sched_us = []            # scheduler time per handled event (host, microseconds)
 
     # ---------------------------------------------------------------- partitions
     def _masks(self, stage):
@@ -214,6 +216,7 @@ class Server:
                     batch.append(waiting.pop(0))
                 if not batch:
                     continue
+                self.decode_batches.append(len(batch))
                 self._decode_step(batch)
                 for r in [r for r in batch if r.done]:
                     batch.remove(r)
@@ -250,6 +253,7 @@ class Server:
                 ev, r = self.events.get(timeout=min(timeout, 0.05))
             except queue.Empty:
                 continue
+            t_ev = time.perf_counter()
             if ev == "vision_done":
                 busy["vision"] = False
                 busy["prefill"] = True            # prefill goes first, before any further vision
@@ -273,12 +277,13 @@ class Server:
                     self.decode_active -= 1
                 self.blocks.give(r.blocks)
                 finished += 1
+            self.sched_us.append((time.perf_counter() - t_ev) * 1e6)
         stop.set()
         vq.put(None)
         pq.put(None)
         for t in threads:
             t.join(timeout=30)
-        return summarize(trace)
+        return self._summary(trace)
 
     def _run_sliced(self, trace):
         t0 = time.perf_counter()
@@ -294,6 +299,7 @@ class Server:
             while q_decode and len(batch) < self.max_batch:   # join at a step boundary
                 batch.append(q_decode.pop(0))
             if batch and (not last_was_decode or (not q_prefill and not q_vision)):
+                self.decode_batches.append(len(batch))
                 self._decode_step(batch)
                 last_was_decode = True
                 for r in [r for r in batch if r.done]:
@@ -319,16 +325,35 @@ class Server:
                 continue
             if pending:
                 time.sleep(max(0.0, min(0.002, pending[0].arrival - (time.perf_counter() - t0))))
-        return summarize(trace)
+        return self._summary(trace)
+
+    def _summary(self, trace):
+        out = summarize(trace)
+        bs = np.array(self.decode_batches or [0])
+        out["decode_steps"] = int(len(self.decode_batches))
+        out["avg_decode_batch"] = round(float(bs.mean()), 3)
+        if self.sched_us:
+            us = np.array(self.sched_us)
+            out["sched_event_us"] = {"p50": round(float(np.percentile(us, 50)), 1), "p99": round(float(np.percentile(us, 99)), 1),
+                                     "max": round(float(us.max()), 1), "events": int(len(us))}
+        return out
 
 
-def summarize(trace):
+def summarize(trace, rate=None):
+    """Latency and throughput of a finished trace.  The vision queue wait (arrival to the start of
+    encode) is set beside Eq. 6's M/G/1 prediction from the measured service times T = encode +
+    prefill (first moment and second moment) at the trace's arrival rate."""
     e2e = np.array([r.t_tokens[-1] - r.t_arrive for r in trace])
     ttft = np.array([r.t_pre1 - r.t_arrive for r in trace])
     tbt = np.array([np.mean(np.diff(r.t_tokens)) if len(r.t_tokens) > 1 else 0.0 for r in trace])
     qwait = np.array([r.t_vis0 - r.t_arrive for r in trace])
+    service = np.array([r.t_pre1 - r.t_vis0 for r in trace])
     span = max(r.t_tokens[-1] for r in trace) - min(r.t_arrive for r in trace)
+    lam = rate if rate is not None else len(trace) / max(trace[-1].arrival, 1e-9)
+    pred = sched.mg1_wait(lam, float(service.mean()), float((service ** 2).mean()))
     return {"requests": len(trace), "max_e2e_s": round(float(e2e.max()), 4), "avg_e2e_s": round(float(e2e.mean()), 4),
             "p50_e2e_s": round(float(np.median(e2e)), 4), "avg_ttft_s": round(float(ttft.mean()), 4),
             "avg_tbt_ms": round(float(tbt.mean()) * 1e3, 3), "max_tbt_ms": round(float(tbt.max()) * 1e3, 3),
-            "avg_queue_wait_s": round(float(qwait.mean()), 4), "throughput_req_s": round(len(trace) / span, 3)}
+            "avg_queue_wait_s": round(float(qwait.mean()), 4), "throughput_req_s": round(len(trace) / span, 3),
+            "mean_service_s": round(float(service.mean()), 4),
+            "eq6_predicted_wait_s": None if pred == float("inf") else round(pred, 4)}

@@ -74,3 +74,13 @@ def test_best_under_load_matches_eq1_plus_eq6():
     lo, hi = sched.best_under_load(c, 32, 0.1), sched.best_under_load(c, 32, 6.0)
     assert hi[0] + hi[1] <= lo[0] + lo[1]
     assert sched.queue_wait(0.2, 5.0) == float("inf")
+
+
+def test_mg1_wait_matches_oracle():
+    # Eq. 6 with measured first and second moments of the service time, and the saturated case
+    for lam, t, t2 in [(2.0, 0.1, 0.012), (4.0, 0.2, 0.05), (0.5, 1.0, 1.5), (3.9, 0.25, 0.07)]:
+        want = osched.mg1_wait(lam, t, t2)
+        assert abs(sched.mg1_wait(lam, t, t2) - want) <= 1e-12 * max(1.0, abs(want))
+    assert sched.mg1_wait(4.0, 0.25, 0.1) == float("inf")
+    # deterministic service reduces to the fixed-T form used by the rate-aware search
+    assert abs(sched.mg1_wait(3.0, 0.2, 0.04) - sched.queue_wait(0.2, 3.0)) < 1e-12

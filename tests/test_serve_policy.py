@@ -80,6 +80,12 @@ def test_alg1_policy(mode):
     assert max(len(b) for b in batches) > 1                              # in-flight batching happened
     assert srv.blocks.free and len(srv.blocks.free) == 2000             # every KV block returned
     assert res["max_e2e_s"] >= res["avg_e2e_s"] > 0
+    # statistics: decode batch sizes of every step, Eq. 6 beside the measured vision-queue wait
+    assert res["decode_steps"] == len(batches)
+    assert abs(res["avg_decode_batch"] - sum(len(b) for b in batches) / len(batches)) < 1e-3
+    assert res["mean_service_s"] > 0 and "eq6_predicted_wait_s" in res
+    if mode == "nova":
+        assert res["sched_event_us"]["events"] >= 2 * len(trace)
 
 
 def test_block_pool_exhaustion_is_an_error():
