@@ -269,7 +269,9 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
 
   const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
   const int total = nm * nn;
-  int id = blockIdx.x;
+  // split K: workgroup blockIdx.x / total takes K slice number that many, writing fp32 partials
+  const int ks = p.kslice ? blockIdx.x / total : 0;
+  int id = blockIdx.x - ks * total;
   if ((total & 7) == 0) id = (id & 7) * (total >> 3) + (id >> 3);
   // groups of G M-tiles sweep the N tiles together (an XCD's ~32 resident tiles then share a few
   // A and W panels in its L2); measured best at 16 for 256-row tiles and 8 for 128-row tiles
@@ -283,7 +285,8 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
   // DMA sources: lane l of a group fills row 8q + l/8, slot l%8 with piece (l%8) ^ ((row/2)%8)
-  const bf16_t* A = reinterpret_cast<const bf16_t*>(p.A);
+  const size_t k_off = (size_t)ks * p.kslice;
+  const bf16_t* A = reinterpret_cast<const bf16_t*>(p.A) + k_off;
   const int lrow = lane >> 3, lslot = lane & 7;
   const bf16_t* asrc[IA];
   const bf16_t* bsrc[IB];
@@ -295,7 +298,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
 #pragma unroll
   for (int t = 0; t < IB; ++t) {
     const int r = (wave * IB + t) * 8 + lrow;
-    bsrc[t] = p.W + (size_t)(n0 + r) * p.ldw + 8 * (lslot ^ ((r >> 1) & 7));
+    bsrc[t] = p.W + k_off + (size_t)(n0 + r) * p.ldw + 8 * (lslot ^ ((r >> 1) & 7));
   }
   auto dma = [&](int kt, int stage) {
     bf16_t* a = lds + stage * STAGE;
@@ -321,7 +324,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   const int sw = (fr >> 1) & 7;
   const int off0 = fr * BK + 8 * (fk ^ sw);          // elements, sub-step 0
   const int off1 = fr * BK + 8 * ((fk + 4) ^ sw);    // sub-step 1
-  const int nk = p.K / BK;
+  const int nk = (p.kslice ? p.kslice : p.K) / BK;
   dma(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -357,7 +360,45 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
     __syncthreads();
   }
 
+  if constexpr (EPI == EPI_STORE && sizeof(OT) == 4) {
+    if (p.kslice) {                    // a K slice: plain fp32 partial tile, no bias
+      GemmArgs q = p;
+      q.out = reinterpret_cast<float*>(p.out) + (size_t)ks * p.split_stride;
+      q.bias = nullptr;
+      gemm_epilogue<OT, EPI, WM, WN>(q, acc, reinterpret_cast<float*>(smem), wave, lane, m0 + wm * WM, n0 + wn * WN);
+      return;
+    }
+  }
   gemm_epilogue<OT, EPI, WM, WN>(p, acc, reinterpret_cast<float*>(smem), wave, lane, m0 + wm * WM, n0 + wn * WN);
+}
+
+// Sum of the K-slice partials in slice order, then the epilogue: STORE out = OT(sum + bias),
+// RESID out += sum + bias (fp32).  One thread per 4 consecutive outputs.
+template <typename OT, int EPI>
+__global__ void __launch_bounds__(256) split_reduce_kernel(GemmArgs p, const float* __restrict__ part, int slices) {
+  const long i4 = (long)blockIdx.x * 256 + threadIdx.x;
+  const int n4 = p.N / 4;
+  if (i4 >= (long)p.M * n4) return;
+  const int m = (int)(i4 / n4), n = (int)(i4 % n4) * 4;
+  const size_t stride = (size_t)p.M * p.N;
+  float4 v = *reinterpret_cast<const float4*>(part + (size_t)m * p.N + n);
+  for (int s = 1; s < slices; ++s) {
+    const float4 w = *reinterpret_cast<const float4*>(part + s * stride + (size_t)m * p.N + n);
+    v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+  }
+  if (p.bias) {
+    const uint2 bb = *reinterpret_cast<const uint2*>(p.bias + n);
+    v.x += bf2f((bf16_t)(bb.x & 0xffff)); v.y += bf2f((bf16_t)(bb.x >> 16));
+    v.z += bf2f((bf16_t)(bb.y & 0xffff)); v.w += bf2f((bf16_t)(bb.y >> 16));
+  }
+  if constexpr (EPI == EPI_RESID) {
+    float4* o = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.out) + (size_t)m * p.ldo + n);
+    const float4 x = *o;
+    *o = float4{x.x + v.x, x.y + v.y, x.z + v.z, x.w + v.w};
+  } else {
+    const float o4[4] = {v.x, v.y, v.z, v.w};
+    store4<OT>(reinterpret_cast<OT*>(p.out) + (size_t)m * p.ldo + n, o4);
+  }
 }
 
 template <typename TA, typename OT, int EPI, int BM, int BN, int WM, int WN>
@@ -380,7 +421,7 @@ static hipError_t launch_tile(const GemmArgs& p, hipStream_t s) {
 }
 
 template <typename OT, int EPI, int BM, int BN, int WM, int WN>
-static hipError_t launch_dma(const GemmArgs& p, hipStream_t s) {
+static hipError_t launch_dma(const GemmArgs& p, hipStream_t s, int kslices = 1) {
   constexpr size_t lds = (size_t)2 * (BM + BN) * BK * sizeof(bf16_t);
   static_assert((size_t)(BM / WM) * (BN / WN) * 16 * (WN + 4) * 4 <= lds, "epilogue scratch exceeds the stages");
   auto kern = gemm_dma_kernel<OT, EPI, BM, BN, WM, WN>;
@@ -392,14 +433,53 @@ static hipError_t launch_dma(const GemmArgs& p, hipStream_t s) {
     attr_set = true;
   }
   const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
-  hipLaunchKernelGGL(kern, dim3(nm * nn), dim3((BM / WM) * (BN / WN) * 64), lds, s, p);
+  hipLaunchKernelGGL(kern, dim3(nm * nn * kslices), dim3((BM / WM) * (BN / WN) * 64), lds, s, p);
   return hipGetLastError();
+}
+
+// K slices for a problem whose 128x128 tiles leave most of a last round idle: slices of at least
+// 1024 along K, a multiple of 64, chosen to fill whole rounds of 2 workgroups per CU best.
+static int split_slices(const GemmArgs& p) {
+  if (!p.split_ws) return 1;
+  const long tiles = (long)((p.M + 127) / 128) * (p.N / 128);
+  const long slots = 512;                         // 256 CUs, 2 workgroups each
+  if (tiles >= 2 * slots) return 1;
+  int best = 1;
+  double best_eff = (double)tiles / (double)(((tiles + slots - 1) / slots) * slots);
+  for (int sl = 2; sl <= 4; ++sl) {
+    if (p.K % (64 * sl) || p.K / sl < 1024) continue;
+    if ((size_t)sl * p.M * p.N > p.split_ws_floats) continue;
+    const long u = tiles * sl;
+    const double eff = (double)u / (double)(((u + slots - 1) / slots) * slots);
+    if (eff > best_eff + 0.05) { best = sl; best_eff = eff; }
+  }
+  return best;
 }
 
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when there are at least two tiles per
-  // CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU).
+  // CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU), with K split into slices
+  // when those tiles cannot fill the GPU (and the caller gave a workspace).
+  if constexpr (sizeof(TA) == 2 && (EPI == EPI_STORE || EPI == EPI_RESID)) {
+    const long tiles256 = (long)((p.M + 255) / 256) * (p.N / 256);
+    if (!(p.N % 256 == 0 && tiles256 >= 512)) {
+      const int sl = split_slices(p);
+      if (sl > 1) {
+        GemmArgs q = p;
+        q.out = p.split_ws;
+        q.ldo = p.N;
+        q.kslice = p.K / sl;
+        q.split_stride = (long)p.M * p.N;
+        hipError_t e = launch_dma<float, EPI_STORE, 128, 128, 64, 64>(q, s, sl);
+        if (e != hipSuccess) return e;
+        const long n4 = (long)p.M * (p.N / 4);
+        hipLaunchKernelGGL((split_reduce_kernel<OT, EPI>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, p,
+                           (const float*)p.split_ws, sl);
+        return hipGetLastError();
+      }
+    }
+  }
   if constexpr (sizeof(TA) == 2) {
     const long tiles = (long)((p.M + 255) / 256) * (p.N / 256);
     if (p.N % 256 == 0 && tiles >= 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);

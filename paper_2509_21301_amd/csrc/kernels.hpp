@@ -23,6 +23,12 @@ struct GemmArgs {
   const bf16_t* bias;
   void* out; int ldo;
   const bf16_t* pos; int pos_rows;
+  // optional split-K workspace: with too few output tiles to fill the GPU, the K range is cut
+  // into up to 4 slices whose fp32 partial products land here ([slices][M][N]) and one more pass
+  // sums them in slice order and applies the epilogue (STORE and RESID only)
+  float* split_ws = nullptr; size_t split_ws_floats = 0;
+  // set by the launcher, not by callers: K slice per workgroup and partial stride
+  int kslice = 0; long split_stride = 0;
 };
 template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s);

@@ -542,6 +542,11 @@ extern "C" size_t nova_kv_bytes(const nova_llm* m, int num_blocks) {
 }
 
 namespace {
+// Split-K partials of the prefill projections: up to 4 K slices of the widest split output.
+size_t prefill_split_floats(const nova_llm* m, int S) {
+  return (size_t)4 * S * std::max<size_t>(m->d.cfg.hidden, m->qkvw);
+}
+
 template <typename T>
 size_t prefill_ws(const nova_llm* m, int S, Carve* cv) {
   const nova_llm_config& c = m->d.cfg;
@@ -555,6 +560,7 @@ size_t prefill_ws(const nova_llm* m, int S, Carve* cv) {
   w.take<T>((size_t)S * c.n_q * c.head_dim);                     // attention out
   w.take<T>((size_t)S * m->ip);                                  // MLP hidden
   w.take<unsigned long long>(1);                                 // argmax key
+  w.take<float>(prefill_split_floats(m, S));                     // split-K partials
   return w.used;
 }
 template <typename T>
@@ -629,7 +635,15 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
   T* att = w.take<T>((size_t)S * qd);
   T* hm = w.take<T>((size_t)S * m->ip);
   unsigned long long* keys = w.take<unsigned long long>(1);
+  const size_t split_floats = prefill_split_floats(m, S);
+  float* split_ws = w.take<float>(split_floats);
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
+  // the QKV, O and down projections may split K when their tiles cannot fill the GPU
+  auto with_split = [&](GemmArgs p) {
+    p.split_ws = split_ws;
+    p.split_ws_floats = split_floats;
+    return p;
+  };
 
   CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(vis, n_vis, ids, n_text, (const bf16_t*)m->d.embed, H, x, s));
   for (int l = 0; l < c.layers; ++l) {
@@ -639,7 +653,7 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
     T* vp = (T*)kv->v + l * kv_layer;
     CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, S, H, W(0), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
     {
-      GemmArgs p{a, H, W(1), H, S, m->qkvw, H, nullptr, qkv, m->qkvw, nullptr, 0};
+      const GemmArgs p = with_split(GemmArgs{a, H, W(1), H, S, m->qkvw, H, nullptr, qkv, m->qkvw, nullptr, 0});
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_STORE, s)));
     }
     CALL(NOVA_KIND_MISC, s, nova::qkv_prefill<T>(qkv, S, 1, c.n_q, c.n_kv, D, c.rope_theta, 0, vt, skp, kp, vp, table, c.block, s));
@@ -648,7 +662,7 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
       CALL(NOVA_KIND_ATTN, s, nova::attention<T>(p, D, s));
     }
     {
-      GemmArgs p{att, qd, W(2), qd, S, H, qd, nullptr, x, H, nullptr, 0};
+      const GemmArgs p = with_split(GemmArgs{att, qd, W(2), qd, S, H, qd, nullptr, x, H, nullptr, 0});
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
     }
     CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, S, H, W(3), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
@@ -657,7 +671,7 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_SWIGLU, s)));
     }
     {
-      GemmArgs p{hm, m->ip, W(5), m->ip, S, H, m->ip, nullptr, x, H, nullptr, 0};
+      const GemmArgs p = with_split(GemmArgs{hm, m->ip, W(5), m->ip, S, H, m->ip, nullptr, x, H, nullptr, 0});
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
     }
   }
