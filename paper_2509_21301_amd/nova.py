@@ -344,6 +344,10 @@ class Llm:
     def _workspace(self, key, nbytes):
         t = self._ws.get(key)
         if t is None or t.numel() < nbytes:
+            if t is not None:
+                # the old buffer may still be in use by work queued on another stream than the one
+                # torch's allocator files it under: let that work finish before it is released
+                torch.cuda.synchronize(self.device)
             t = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
             self._ws[key] = t
         return t
