@@ -50,6 +50,64 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x4 (&a
   // this lane's columns are the same in every pass: 4 consecutive ones, or for SwiGLU (W rows
   // interleaved in blocks of 8: of each 16 columns, 0-7 gate and 8-15 the matching up rows)
   // 4 gate columns and the 4 up columns 8 further, giving 4 outputs
+  if constexpr (EPI == EPI_STORE) {
+    if (p.vt != nullptr && col0 >= p.v_col0) {
+      // V columns of a fused QKV projection go to V^T.  bf16: 64 columns at a time are staged in
+      // the wave's LDS scratch transposed ([column][WM tokens + 8], each lane writing its 4
+      // consecutive tokens of one column as 8 bytes), then every V^T row segment of WM tokens
+      // leaves as whole 16-byte pieces.  fp32 (exact mode): one 16-byte store per lane and tile.
+      const int er = (lane >> 4) * 4, ec = lane & 15;
+      const int heads = (p.N - p.v_col0) / p.vt_hd;
+      OT* vt = reinterpret_cast<OT*>(p.vt);
+      if constexpr (sizeof(OT) == 2) {
+        constexpr int TP = WM + 8;                 // bf16 pitch of a staged column
+        constexpr int TN2 = TN < 4 ? TN : 4;       // 16-column blocks per pass
+        constexpr int CH = WM / 8;                 // 16-byte pieces per staged column
+        bf16_t* tl = reinterpret_cast<bf16_t*>(smem) + wave * (TN2 * 16) * TP;
+#pragma unroll
+        for (int jh = 0; jh < TN; jh += TN2) {
+#pragma unroll
+          for (int j = 0; j < TN2; ++j) {
+            const int n = col0 + (jh + j) * 16 + ec;
+            const float bv = p.bias ? bf2f(p.bias[n]) : 0.f;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+              *reinterpret_cast<uint2*>(tl + (j * 16 + ec) * TP + i * 16 + er) =
+                  make_uint2(pack2(acc[i][jh + j][0] + bv, acc[i][jh + j][1] + bv),
+                             pack2(acc[i][jh + j][2] + bv, acc[i][jh + j][3] + bv));
+          }
+          asm volatile("" ::: "memory");     // a wave's LDS operations execute in order
+#pragma unroll
+          for (int q = lane; q < TN2 * 16 * CH; q += 64) {
+            const int cc = q / CH, m = row0 + (q % CH) * 8;     // 8 tokens, never across images
+            if (m < p.M) {
+              const int b = m / p.vt_tokens, t = m - b * p.vt_tokens;
+              const int c = col0 + jh * 16 + cc - p.v_col0, h = c / p.vt_hd, d = c - h * p.vt_hd;
+              *reinterpret_cast<u32x4*>(vt + ((size_t)(b * heads + h) * p.vt_hd + d) * p.vt_pad + t) =
+                  *reinterpret_cast<const u32x4*>(tl + cc * TP + (q % CH) * 8);
+            }
+          }
+          asm volatile("" ::: "memory");
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int m = row0 + i * 16 + er;
+          if (m >= p.M) continue;
+          const int b = m / p.vt_tokens, t = m - b * p.vt_tokens;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int n = col0 + j * 16 + ec, c = n - p.v_col0;
+            const int h = c / p.vt_hd, d = c - h * p.vt_hd;
+            const float bv = p.bias ? bf2f(p.bias[n]) : 0.f;
+            const float o[4] = {acc[i][j][0] + bv, acc[i][j][1] + bv, acc[i][j][2] + bv, acc[i][j][3] + bv};
+            store4<OT>(vt + ((size_t)(b * heads + h) * p.vt_hd + d) * p.vt_pad + t, o);
+          }
+        }
+      }
+      return;
+    }
+  }
   const int c = SW ? (q >> 1) * 16 + (q & 1) * 4 : q * 4;
   const int n = col0 + c;
   const int nout = SW ? (col0 >> 1) + (q >> 1) * 8 + (q & 1) * 4 : n;
@@ -471,6 +529,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         q.ldo = p.N;
         q.kslice = p.K / sl;
         q.split_stride = (long)p.M * p.N;
+        q.vt = nullptr;
         hipError_t e = launch_dma<float, EPI_STORE, 128, 128, 64, 64>(q, s, sl);
         if (e != hipSuccess) return e;
         const long n4 = (long)p.M * (p.N / 4);

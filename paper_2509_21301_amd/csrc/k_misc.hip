@@ -432,6 +432,24 @@ template hipError_t norm_rows<bf16_t>(const float*, int, int, const bf16_t*, con
 template hipError_t norm_rows<float>(const float*, int, int, const bf16_t*, const bf16_t*, float, int, float*, int, int, int, int, hipStream_t);
 template hipError_t patchify<bf16_t>(const bf16_t*, int, int, int, int, int, bf16_t*, hipStream_t);
 template hipError_t patchify<float>(const bf16_t*, int, int, int, int, int, float*, hipStream_t);
+template <typename T>
+__global__ void zero_tail_cols_kernel(T* __restrict__ buf, long rows, int ld, int c0) {
+  const int w = ld - c0;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < rows * w; i += (long)gridDim.x * blockDim.x)
+    buf[(i / w) * ld + c0 + i % w] = T(0);
+}
+
+template <typename T>
+hipError_t zero_tail_cols(T* buf, long rows, int ld, int c0, hipStream_t s) {
+  if (rows <= 0 || c0 >= ld) return hipSuccess;
+  const long n = rows * (ld - c0);
+  hipLaunchKernelGGL((zero_tail_cols_kernel<T>), dim3((unsigned)std::min<long>((n + 255) / 256, 4096)), dim3(256), 0, s,
+                     buf, rows, ld, c0);
+  return hipGetLastError();
+}
+template hipError_t zero_tail_cols<bf16_t>(bf16_t*, long, int, int, hipStream_t);
+template hipError_t zero_tail_cols<float>(float*, long, int, int, hipStream_t);
+
 template hipError_t qkv_prefill<bf16_t>(bf16_t*, int, int, int, int, int, float, int, bf16_t*, int, bf16_t*, bf16_t*, const int*, int, hipStream_t);
 template hipError_t qkv_prefill<float>(float*, int, int, int, int, int, float, int, float*, int, float*, float*, const int*, int, hipStream_t);
 template hipError_t qkv_decode<bf16_t>(const float*, int, int, int, int, int, float, const int*, bf16_t*, bf16_t*, bf16_t*, const int*, int, int, hipStream_t);

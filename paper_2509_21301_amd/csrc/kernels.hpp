@@ -29,6 +29,11 @@ struct GemmArgs {
   float* split_ws = nullptr; size_t split_ws_floats = 0;
   // set by the launcher, not by callers: K slice per workgroup and partial stride
   int kslice = 0; long split_stride = 0;
+  // optional, STORE only: output columns from v_col0 on (the V of a fused QKV projection) go
+  // transposed to vt instead of out: column v_col0 + h * vt_hd + d of row m = b * vt_tokens + t
+  // lands at vt[((b * heads + h) * vt_hd + d) * vt_pad + t].  Requires v_col0 % 256 == 0,
+  // vt_tokens % 8 == 0 and vt_pad % 8 == 0 (checked by the caller).
+  void* vt = nullptr; int v_col0 = 0, vt_hd = 0, vt_tokens = 0, vt_pad = 0;
 };
 template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s);
@@ -110,6 +115,9 @@ hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t
 // Image [B, H, W, 3] bf16 -> patch rows [B*gh*gw, kpad] (zero padded), order (py, px, c).
 template <typename T>
 hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* out, hipStream_t s);
+// Zero columns [c0, ld) of `rows` rows of pitch ld (the key padding of a V^T buffer).
+template <typename T>
+hipError_t zero_tail_cols(T* buf, long rows, int ld, int c0, hipStream_t s);
 // Split a packed QKV projection.  Rotates q and k in place when rope_theta > 0 (positions
 // pos0 + t), writes V transposed for attention (vt), and when tables != null writes the
 // rotated K and V of every token into the paged cache.

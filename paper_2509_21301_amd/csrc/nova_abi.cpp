@@ -429,6 +429,10 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
     CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_POS, s)));
   }
   const int L = c.layers, K = v->offload ? v->d.n_slots : 0;
+  // the QKV projection writes V^T itself when V starts on a 256-column tile and tokens come in
+  // eights; the keys past N then stay zero for the whole pass
+  const bool vt_fused = (2 * H) % 256 == 0 && N % 8 == 0;
+  if (vt_fused) CALL(NOVA_KIND_MISC, s, nova::zero_tail_cols<T>(vt, (long)B * H, skp, N, s));
   // the first K layers: already in their slots after an earlier call (its tail loaded them), else
   // all K copies are queued here at once rather than one per layer
   for (int l = 0; l < K; ++l)
@@ -451,9 +455,13 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
     CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, M, H, W(0), W(1), c.eps, 1, a, H, 1, 0, 0, s));
     {
       GemmArgs p{a, H, W(2), H, M, 3 * H, H, W(3), qkv, 3 * H, nullptr, 0};
+      if (vt_fused) {      // V straight to V^T from the projection's epilogue
+        p.vt = vt, p.v_col0 = 2 * H, p.vt_hd = hd, p.vt_tokens = N, p.vt_pad = skp;
+      }
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_STORE, s)));
     }
-    CALL(NOVA_KIND_MISC, s, nova::qkv_prefill<T>(qkv, N, B, heads, heads, hd, 0.f, 0, vt, skp, nullptr, nullptr, nullptr, 16, s));
+    if (!vt_fused)
+      CALL(NOVA_KIND_MISC, s, nova::qkv_prefill<T>(qkv, N, B, heads, heads, hd, 0.f, 0, vt, skp, nullptr, nullptr, nullptr, 16, s));
     {
       nova::AttnArgs p{qkv, 3L * H, (long)N * 3 * H, qkv + H, 3L * H, (long)N * 3 * H, vt, skp, att, H, (long)N * H,
                        N, N, heads, heads, B, 0};
