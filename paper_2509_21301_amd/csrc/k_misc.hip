@@ -16,7 +16,9 @@ namespace nova {
 // outputs at a time.  merge > 1 scatters row (image, py, px) of a gh x gw patch grid to the
 // merged token it belongs to, at column block (py % merge) * merge + px % merge.
 constexpr int NORM_MAXV = 16;     // float4 per lane: H <= 64 * 4 * 16
-template <typename T>
+// NV: float4 per lane held in registers (the row width rounded up to 256 columns), as few as the
+// row needs so that more rows are in flight per CU
+template <typename T, int NV>
 __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, int M, int H, const bf16_t* __restrict__ g,
                                                    const bf16_t* __restrict__ bb, float eps, int ln, T* __restrict__ out,
                                                    int ldo, int merge, int gh, int gw) {
@@ -25,10 +27,10 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
   if (row >= M) return;
   const float4* xr = reinterpret_cast<const float4*>(x + (size_t)row * H);
   const int n4 = H / 4;
-  float4 v[NORM_MAXV];
+  float4 v[NV];
   float s = 0.f;
 #pragma unroll
-  for (int j = 0; j < NORM_MAXV; ++j) {
+  for (int j = 0; j < NV; ++j) {
     const int i = j * 64 + lane;
     v[j] = i < n4 ? xr[i] : float4{0.f, 0.f, 0.f, 0.f};
     s += v[j].x + v[j].y + v[j].z + v[j].w;
@@ -36,7 +38,7 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
   const float mean = ln ? wave_sum(s) / H : 0.f;
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < NORM_MAXV; ++j) {
+  for (int j = 0; j < NV; ++j) {
     if (j * 64 + lane < n4) {
       const float a = v[j].x - mean, b = v[j].y - mean, c = v[j].z - mean, d = v[j].w - mean;
       ss += a * a + b * b + c * c + d * d;
@@ -52,7 +54,7 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
   }
   T* o = out + orow * ldo + ocol;
 #pragma unroll
-  for (int j = 0; j < NORM_MAXV; ++j) {
+  for (int j = 0; j < NV; ++j) {
     const int i = j * 64 + lane;
     if (i >= n4) continue;
     const uint2 gg = *reinterpret_cast<const uint2*>(g + 4 * i);
@@ -76,7 +78,17 @@ hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t
                      int ldo, int merge, int gh, int gw, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (H % 4 || H > 4 * 64 * NORM_MAXV || ldo % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((norm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, g, b, eps, ln, out, ldo, merge, gh, gw);
+  const dim3 grid((M + 3) / 4);
+  const int nv = (H + 255) / 256;
+#define NORM_LAUNCH(NVV) hipLaunchKernelGGL((norm_kernel<T, NVV>), grid, dim3(256), 0, s, x, M, H, g, b, eps, ln, out, ldo, merge, gh, gw)
+  if (nv <= 1) NORM_LAUNCH(1);
+  else if (nv <= 2) NORM_LAUNCH(2);
+  else if (nv <= 4) NORM_LAUNCH(4);
+  else if (nv <= 5) NORM_LAUNCH(5);
+  else if (nv <= 8) NORM_LAUNCH(8);
+  else if (nv <= 14) NORM_LAUNCH(14);
+  else NORM_LAUNCH(NORM_MAXV);
+#undef NORM_LAUNCH
   return hipGetLastError();
 }
 
