@@ -540,8 +540,28 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
     }
   }
   if constexpr (sizeof(TA) == 2) {
-    const long tiles = (long)((p.M + 255) / 256) * (p.N / 256);
-    if (p.N % 256 == 0 && tiles >= 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
+    const int nm = (p.M + 255) / 256;
+    const long tiles = (long)nm * (p.N / 256);
+    if (p.N % 256 == 0 && tiles >= 512) {
+      // few row tiles and many column tiles (the prefill's gate/up projection: 6 x 148): the
+      // columns of whole rounds of 256x256 tiles, then the rest with 128x128 tiles, so that the
+      // last round is not left mostly idle
+      const long rounds = tiles / 256;
+      const int n1 = (int)(rounds * 256 / nm) * 256;
+      if (tiles % 256 >= 32 && nm <= 16 && n1 < p.N && EPI != EPI_POS) {
+        GemmArgs a = p;
+        a.N = n1;
+        hipError_t e = launch_dma<OT, EPI, 256, 256, 64, 128>(a, s);
+        if (e != hipSuccess) return e;
+        GemmArgs b = p;
+        b.N = p.N - n1;
+        b.W = p.W + (size_t)n1 * p.ldw;
+        if (p.bias) b.bias = p.bias + n1;
+        b.out = reinterpret_cast<OT*>(p.out) + (EPI == EPI_SWIGLU ? n1 / 2 : n1);
+        return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
+      }
+      return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
+    }
     return launch_dma<OT, EPI, 128, 128, 64, 64>(p, s);
   }
   return launch_tile<TA, OT, EPI, 128, 128, 64, 64>(p, s);
