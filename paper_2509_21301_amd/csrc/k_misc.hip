@@ -121,22 +121,43 @@ hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* 
 }
 
 // ------------------------------------------------------------------ rotary embedding in place
-// Half-split pairing: (c, c + D/2) rotate by angle pos * theta^(-2c/D).
+// Half-split pairing: (c, c + D/2) rotate by angle pos * theta^(-2c/D).  A thread takes one
+// 16-byte piece of each half (8 bf16 or 4 fp32 pairs); the inverse frequencies are computed once
+// per workgroup, and each angle is formed and reduced in double before the fp32 sine/cosine, as
+// in the decode kernel.
 template <typename T>
-__global__ void rope_inplace_kernel(T* __restrict__ qkv, int rows, int S, int n_rot_heads, int D, float theta, int pos0, int ld) {
+__global__ void __launch_bounds__(256) rope_inplace_kernel(T* __restrict__ qkv, int rows, int S, int n_rot_heads, int D,
+                                                           float theta, int pos0, int ld) {
+  constexpr int V = 16 / sizeof(T);
+  __shared__ double inv_s[64];                       // D / 2 <= 64
   const int half = D / 2;
-  const long total = (long)rows * n_rot_heads * half;
+  for (int c = threadIdx.x; c < half; c += blockDim.x) inv_s[c] = exp2(-(2.0 * c / D) * log2((double)theta));
+  __syncthreads();
+  const int pieces = half / V;
+  const long total = (long)rows * n_rot_heads * pieces;
   for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
-    const int c = (int)(idx % half);
-    const long t = idx / half;
+    const int pc = (int)(idx % pieces);
+    const long t = idx / pieces;
     const int hh = (int)(t % n_rot_heads);
     const int row = (int)(t / n_rot_heads);
-    float sn, cs;
-    rope_sincos(pos0 + row % S, c, D, theta, &sn, &cs);
-    T* e = qkv + (size_t)row * ld + (size_t)hh * D;
-    const float x1 = to_f<T>(e[c]), x2 = to_f<T>(e[c + half]);
-    e[c] = from_f<T>(x1 * cs - x2 * sn);
-    e[c + half] = from_f<T>(x2 * cs + x1 * sn);
+    const double pos = (double)(pos0 + row % S);
+    T* e1 = qkv + (size_t)row * ld + (size_t)hh * D + pc * V;
+    T* e2 = e1 + half;
+    T a[V], bv[V];
+    *reinterpret_cast<u32x4*>(a) = *reinterpret_cast<const u32x4*>(e1);
+    *reinterpret_cast<u32x4*>(bv) = *reinterpret_cast<const u32x4*>(e2);
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      double ang = pos * inv_s[pc * V + v];
+      ang -= 6.283185307179586 * floor(ang * 0.15915494309189535);
+      float sn, cs;
+      sincosf((float)ang, &sn, &cs);
+      const float x1 = to_f<T>(a[v]), x2 = to_f<T>(bv[v]);
+      a[v] = from_f<T>(x1 * cs - x2 * sn);
+      bv[v] = from_f<T>(x2 * cs + x1 * sn);
+    }
+    *reinterpret_cast<u32x4*>(e1) = *reinterpret_cast<const u32x4*>(a);
+    *reinterpret_cast<u32x4*>(e2) = *reinterpret_cast<const u32x4*>(bv);
   }
 }
 
@@ -194,10 +215,10 @@ template <typename T>
 hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0, T* vt,
                        int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s) {
   if (S <= 0) return hipSuccess;
-  if (D > 128 || D % 8 || sk_pad < S || sk_pad % 64) return hipErrorInvalidValue;
+  if (D > 128 || D % 16 || sk_pad < S || sk_pad % 64) return hipErrorInvalidValue;
   const int ld = (n_q + 2 * n_kv) * D;
   if (rope_theta > 0.f) {
-    const long total = (long)batch * S * (n_q + n_kv) * (D / 2);
+    const long total = (long)batch * S * (n_q + n_kv) * (D / 2 / (16 / (int)sizeof(T)));
     const int grid = (int)std::min<long>((total + 255) / 256, 65536);
     hipLaunchKernelGGL((rope_inplace_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, batch * S, S, n_q + n_kv, D,
                        rope_theta, pos0, ld);
