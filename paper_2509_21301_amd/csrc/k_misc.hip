@@ -193,21 +193,28 @@ __global__ void __launch_bounds__(256) kv_scatter_kernel(const T* __restrict__ q
 #pragma unroll
     for (int j = 0; j < EPC; ++j) vals[j] = tile[(tc + j) * TP + d];
     *reinterpret_cast<u32x4*>(vdst + (size_t)d * sk_pad + t0 + tc) = *reinterpret_cast<const u32x4*>(vals);
+    // the same EPC keys of row d also form one piece of the paged V block ([d][slot] layout);
+    // EPC divides the block, so the piece never straddles two blocks
+    if (table != nullptr && t0 + tc < S) {
+      const int tok = t0 + tc, phys = table[tok / block], slot = tok % block;
+      if (tok + EPC <= S) {
+        *reinterpret_cast<u32x4*>(vpool + (((size_t)phys * n_kv + kvh) * D + d) * block + slot) =
+            *reinterpret_cast<const u32x4*>(vals);
+      } else {
+        for (int j = 0; j < S - tok; ++j) vpool[(((size_t)phys * n_kv + kvh) * D + d) * block + slot + j] = vals[j];
+      }
+    }
   }
   if (table == nullptr) return;
-  for (int i = threadIdx.x; i < 64 * D; i += 256) {
-    const int t = i / D, c = i % D;
+  // K rows: D contiguous elements in both layouts, copied 16 bytes at a time
+  const int kc = D / EPC;
+  for (int i = threadIdx.x; i < 64 * kc; i += 256) {
+    const int t = i / kc, c = (i % kc) * EPC;
     const int tok = t0 + t;
     if (tok >= S) continue;
     const int phys = table[tok / block], slot = tok % block;
-    kpool[(((size_t)phys * n_kv + kvh) * block + slot) * D + c] = ksrc[(size_t)tok * ld + c];
-  }
-  for (int i = threadIdx.x; i < 64 * D; i += 256) {
-    const int c = i / 64, t = i % 64;
-    const int tok = t0 + t;
-    if (tok >= S) continue;
-    const int phys = table[tok / block], slot = tok % block;
-    vpool[(((size_t)phys * n_kv + kvh) * D + c) * block + slot] = tile[t * TP + c];
+    *reinterpret_cast<u32x4*>(kpool + (((size_t)phys * n_kv + kvh) * block + slot) * D + c) =
+        *reinterpret_cast<const u32x4*>(ksrc + (size_t)tok * ld + c);
   }
 }
 
