@@ -14,7 +14,9 @@
 //    stored with two 4-key blocks of every 16 swapped so that a fragment is one 16-byte read;
 //  * head_dim 64 / 80 / 128 (80 = 5 k-steps of 16 for QK^T; PV pads the output rows to 96);
 //  * fp32 mode (tiny-stack exact mode): q, k, v, p are split into bf16 hi + lo parts and the
-//    three significant cross products are accumulated.
+//    three significant cross products are accumulated;
+//  * bidirectional bf16 with head_dim <= 80 (the vision encoder) runs a wider variant: two query
+//    groups per wave share every fragment read, and the row sums come out of the P V^T MFMAs.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -276,8 +278,205 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
     }
 }
 
+// Bidirectional bf16 attention with two 32-query groups per wave (256 queries per workgroup):
+// each K and V^T fragment read from LDS feeds two MFMAs, and each K/V tile the workgroup stages
+// serves twice the queries, which halves the LDS and L2 traffic per flop of the kernel above.
+// When the head dimension is padded up to the 32-row MFMA block (d = 80 -> 96), the padding
+// rows of the V^T tile hold ones, so the P V^T product also accumulates each query's sum of
+// (bf16) probabilities, rescaled together with the output: no separate row sum is kept.
+constexpr int AQW = 256;
+
+template <int D>
+__global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
+  constexpr int NS = D / 16;
+  constexpr int DP = (D + 31) / 32 * 32;
+  constexpr int NC = DP / 32;
+  constexpr int KP = D + 8, VP = AK + 8;
+  constexpr bool ONES = DP > D;
+  __shared__ __align__(16) bf16_t ks[AK * KP];
+  __shared__ __align__(16) bf16_t vs[DP * VP];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, lq = lane & 31;
+  const int nqb = (p.sq + AQW - 1) / AQW;
+  int qb, h, b;
+  {
+    const int pairs = p.batch * p.n_q, lin = blockIdx.x;
+    int pair;
+    if (pairs % 8 == 0) {
+      const int j = lin >> 3;
+      pair = (lin & 7) * (pairs >> 3) + j / nqb;
+      qb = j % nqb;
+    } else {
+      pair = lin / nqb;
+      qb = lin % nqb;
+    }
+    h = pair % p.n_q;
+    b = pair / p.n_q;
+  }
+  const int kvh = h / (p.n_q / p.n_kv);
+  const int qbase = qb * AQW + wave * 64;          // group u holds queries qbase + 32 u + lq
+  const bool active = qbase < p.sq;
+
+  const bf16_t* Q = reinterpret_cast<const bf16_t*>(p.q) + (size_t)b * p.q_batch + (size_t)h * D;
+  const bf16_t* K = reinterpret_cast<const bf16_t*>(p.k) + (size_t)b * p.k_batch + (size_t)kvh * D;
+  const bf16_t* VT = reinterpret_cast<const bf16_t*>(p.vt) + ((size_t)b * p.n_kv + kvh) * D * (size_t)p.sk_pad;
+
+  Frag8 qh[2][NS];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int qrow = qbase + 32 * u + lq;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qh[u][s] = qrow < p.sq ? *reinterpret_cast<const Frag8*>(Q + (size_t)qrow * p.q_row + 16 * s + 8 * g) : zero_frag();
+  }
+
+  constexpr int K_CH = AK * D / 8, V_CH = D * AK / 8;
+  constexpr int K_IT = (K_CH + 255) / 256, V_IT = (V_CH + 255) / 256;
+  u32x4 rk[K_IT], rv[V_IT];
+  auto load_tile = [&](int kv0) {
+#pragma unroll
+    for (int i = 0; i < K_IT; ++i) {
+      const int c = min(tid + i * 256, K_CH - 1);
+      const int r = c / (D / 8), col = (c % (D / 8)) * 8;
+      rk[i] = *reinterpret_cast<const u32x4*>(K + (size_t)min(kv0 + r, p.sk - 1) * p.k_row + col);
+    }
+#pragma unroll
+    for (int i = 0; i < V_IT; ++i) {
+      const int c = min(tid + i * 256, V_CH - 1);
+      const int r = c / (AK / 8), col = (c % (AK / 8)) * 8;
+      rv[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)r * p.sk_pad + kv0 + col);
+    }
+  };
+  auto vpos = [](int key) { const int bk = (key >> 2) & 3; return (key & ~15) + 4 * (((bk & 1) << 1) | (bk >> 1)); };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < K_IT; ++i) {
+      const int c = tid + i * 256;
+      if (c < K_CH) {
+        const int r = c / (D / 8), col = (c % (D / 8)) * 8;
+        *reinterpret_cast<u32x4*>(&ks[r * KP + col]) = rk[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < V_IT; ++i) {
+      const int c = tid + i * 256;
+      if (c < V_CH) {
+        const int r = c / (AK / 8), col = (c % (AK / 8)) * 8;
+        *reinterpret_cast<uint2*>(&vs[r * VP + vpos(col)]) = make_uint2(rv[i][0], rv[i][1]);
+        *reinterpret_cast<uint2*>(&vs[r * VP + vpos(col + 4)]) = make_uint2(rv[i][2], rv[i][3]);
+      }
+    }
+  };
+  if constexpr (ONES) {       // rows D .. DP-1 of the V^T tile: bf16 ones, never overwritten
+    for (int i = tid; i < (DP - D) * VP / 2; i += 256)
+      reinterpret_cast<uint32_t*>(vs + D * VP)[i] = 0x3f803f80u;
+  }
+
+  f32x16 o[2][NC];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) o[u][c] = f32x16{};
+  float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
+  const float scale = 1.4426950408889634f / sqrtf((float)D);
+
+  load_tile(0);
+  for (int kv0 = 0; kv0 < p.sk; kv0 += AK) {
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (kv0 + AK < p.sk) load_tile(kv0 + AK);
+    if (!active) continue;
+
+    // the online softmax advances 32 keys at a time: half the score registers, and the next
+    // block's S^T MFMAs are independent of this block's exponentials
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 sacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const Frag8 ka = *reinterpret_cast<const Frag8*>(&ks[(kb * 32 + lq) * KP + 16 * s + 8 * g]);
+        sacc[0] = mfma32(ka, qh[0][s], sacc[0]);
+        sacc[1] = mfma32(ka, qh[1][s], sacc[1]);
+      }
+      if (kv0 + kb * 32 + 32 > p.sk) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (kv0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3) >= p.sk) sacc[u][r] = -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        float tmax = -1e30f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[u][r]);
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        const float m_new = fmaxf(m_run[u], tmax);
+        const float ms = m_new * scale;
+        float rsum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[u][r], scale, -ms));
+          sacc[u][r] = pv;
+          if constexpr (!ONES) rsum += pv;
+        }
+        if (__ballot(m_new > m_run[u])) {
+          const float corr = __builtin_amdgcn_exp2f((m_run[u] - m_new) * scale);
+#pragma unroll
+          for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[u][c][r] *= corr;
+          if constexpr (!ONES) l_run[u] *= corr;
+        }
+        if constexpr (!ONES) l_run[u] += rsum + __shfl_xor(rsum, 32, 64);
+        m_run[u] = m_new;
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        Frag8 ph[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) ph[u].w[e] = pack2(sacc[u][8 * t + 2 * e], sacc[u][8 * t + 2 * e + 1]);
+        const int kpos = kb * 32 + 16 * t + 8 * g;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const Frag8 va = *reinterpret_cast<const Frag8*>(&vs[(c * 32 + lq) * VP + kpos]);
+          o[0][c] = mfma32(va, ph[0], o[0][c]);
+          o[1][c] = mfma32(va, ph[1], o[1][c]);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int qrow = qbase + 32 * u + lq;
+    if (qrow >= p.sq) continue;
+    // with ONES, element 8 of the last block is output row 32 (NC - 1) + 16 + 4 g: a ones row
+    const float inv = 1.0f / (ONES ? o[u][NC - 1][8] : l_run[u]);
+    bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + (size_t)b * p.o_batch + (size_t)qrow * p.o_row + (size_t)h * D;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + 8 * r4 + 4 * g;
+        if (col >= D) continue;
+        *reinterpret_cast<uint2*>(out + col) =
+            make_uint2(pack2(o[u][c][4 * r4] * inv, o[u][c][4 * r4 + 1] * inv), pack2(o[u][c][4 * r4 + 2] * inv, o[u][c][4 * r4 + 3] * inv));
+      }
+  }
+}
+
 template <typename T, int D>
 static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
+  if constexpr (sizeof(T) == 2 && D <= 80) {
+    if (!p.causal) {
+      hipLaunchKernelGGL((attn_wide_kernel<D>), dim3((p.sq + AQW - 1) / AQW * p.n_q * p.batch), dim3(256), 0, s, p);
+      return hipGetLastError();
+    }
+  }
   dim3 grid((p.sq + AQ - 1) / AQ * p.n_q * p.batch);
   if (p.causal) hipLaunchKernelGGL((attn_kernel<T, D, true>), grid, dim3(256), 0, s, p);
   else hipLaunchKernelGGL((attn_kernel<T, D, false>), grid, dim3(256), 0, s, p);

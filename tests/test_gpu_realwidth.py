@@ -2,7 +2,9 @@
 one by one (through the C ABI, bf16, tolerance 2e-2):
 
 * vision encode: one 1280-wide layer (16 heads of 80, MLP 5120) on two 1008x1008 images
-  (5184 patches each) with the 2x2 merge to 3584 -- sampled merged tokens of both images;
+  (5184 patches each) with the 2x2 merge to 3584 -- sampled merged tokens of both images; and a
+  2-layer encoder with the same head size over 200 patches (a ragged last key tile) -- every
+  merged token;
 * prefill: one 3584-wide GQA layer (28/4 heads of 128, SwiGLU 18944, vocab 152064) over
   1300 visual embeddings + 200 text tokens -- last-row logits, greedy id, sampled K/V;
 * decode: 4 and 20 sequences with ragged contexts of 1200..1500 tokens in a shuffled paged cache
@@ -35,6 +37,23 @@ def test_vit_layer_real_width(gpu_lib):
     for i in range(2):
         ref = vlm.vit_encode_tokens(imgs[i], w, VIT1, tokens)
         assert vlm.max_rel_err(out[i, tokens], ref) < sc.TOL_BF16, f"image {i}"
+
+
+# 8 heads of 80 over a 10x20 patch grid: 200 keys leave a ragged last key tile (3 x 64 + 8) and
+# the 256-query workgroup has two of its four waves idle and one half filled
+VIT_D80 = synth.VitConfig(hidden=640, heads=8, mlp=1280, layers=2, patch=14, merge=2, out_hidden=256,
+                          image_h=140, image_w=280, name="vit2_d80_ragged")
+
+
+def test_vit_head80_ragged_keys(gpu_lib):
+    import torch
+    nova = gpu_lib
+    w = synth.vit_weights(VIT_D80, seed=4)
+    imgs = synth.image(2, VIT_D80.image_h, VIT_D80.image_w, seed=6)
+    out = nova.Vit(VIT_D80, w).encode(torch.from_numpy(imgs).cuda().to(torch.bfloat16)).float().cpu().numpy()
+    for i in range(2):
+        ref = vlm.vit_encode(imgs[i], w, VIT_D80)
+        assert vlm.max_rel_err(out[i], ref) < sc.TOL_BF16, f"image {i}"
 
 
 @pytest.fixture(scope="module")
