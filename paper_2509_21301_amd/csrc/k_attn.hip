@@ -281,10 +281,20 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
 // Bidirectional bf16 attention with two 32-query groups per wave (256 queries per workgroup):
 // each K and V^T fragment read from LDS feeds two MFMAs, and each K/V tile the workgroup stages
 // serves twice the queries, which halves the LDS and L2 traffic per flop of the kernel above.
-// When the head dimension is padded up to the 32-row MFMA block (d = 80 -> 96), the padding
-// rows of the V^T tile hold ones, so the P V^T product also accumulates each query's sum of
-// (bf16) probabilities, rescaled together with the output: no separate row sum is kept.
+//  * K and V^T tiles go global -> LDS by 16-byte LDS-DMA loads into two stages (separate arrays,
+//    the loop unrolled by two so that each stage is addressed statically): the next tile loads
+//    while this one is consumed, with one barrier per tile and no staging registers;
+//  * the K rows of every 16-key group are stored with their middle two 4-row blocks swapped.
+//    The S^T accumulator rows a lane holds are then keys 16t + 8g .. +7 of chunk t, in order,
+//    which is the k range of the P^T operand, so the V^T tile is used in natural key order;
+//  * when the head dimension is padded up to the 32-row MFMA block (d = 80 -> 96), the padding
+//    rows of the V^T tiles hold ones, so the P V^T product also accumulates each query's sum of
+//    (bf16) probabilities, rescaled together with the output: no separate row sum is kept.
 constexpr int AQW = 256;
+
+__device__ __forceinline__ void attn_dma16(const bf16_t* g, bf16_t* l_base) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l_base, 16, 0, 0);
+}
 
 template <int D>
 __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
@@ -292,11 +302,17 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   constexpr int DP = (D + 31) / 32 * 32;
   constexpr int NC = DP / 32;
   constexpr int KP = D + 8, VP = AK + 8;
+  constexpr int KPS = KP / 8, VPS = VP / 8;            // 16-byte slots per LDS row (last one: pad)
+  constexpr int K_INS = (AK * KPS + 63) / 64, V_INS = (D * VPS + 63) / 64;
+  constexpr int K_IW = (K_INS + 3) / 4, V_IW = (V_INS + 3) / 4;   // DMA instructions per wave
   constexpr bool ONES = DP > D;
-  __shared__ __align__(16) bf16_t ks[AK * KP];
-  __shared__ __align__(16) bf16_t vs[DP * VP];
+  __shared__ __align__(16) bf16_t ks0[AK * KP];
+  __shared__ __align__(16) bf16_t vs0[DP * VP];
+  __shared__ __align__(16) bf16_t ks1[AK * KP];
+  __shared__ __align__(16) bf16_t vs1[DP * VP];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, lq = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, lq = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // scalar: uniform branches
   const int nqb = (p.sq + AQW - 1) / AQW;
   int qb, h, b;
   {
@@ -330,46 +346,36 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
       qh[u][s] = qrow < p.sq ? *reinterpret_cast<const Frag8*>(Q + (size_t)qrow * p.q_row + 16 * s + 8 * g) : zero_frag();
   }
 
-  constexpr int K_CH = AK * D / 8, V_CH = D * AK / 8;
-  constexpr int K_IT = (K_CH + 255) / 256, V_IT = (V_CH + 255) / 256;
-  u32x4 rk[K_IT], rv[V_IT];
-  auto load_tile = [&](int kv0) {
+  // DMA instruction i (dealt to wave i % 4) fills LDS slots 64 i .. 64 i + 63 of a tile, slot j
+  // being piece j % (slots per row) of LDS row j / (slots per row); pad slots are masked off
+  int k_row[K_IW], k_col[K_IW], v_off[V_IW];
+  bool k_on[K_IW], v_on[V_IW];
 #pragma unroll
-    for (int i = 0; i < K_IT; ++i) {
-      const int c = min(tid + i * 256, K_CH - 1);
-      const int r = c / (D / 8), col = (c % (D / 8)) * 8;
-      rk[i] = *reinterpret_cast<const u32x4*>(K + (size_t)min(kv0 + r, p.sk - 1) * p.k_row + col);
-    }
+  for (int t = 0; t < K_IW; ++t) {
+    const int ins = wave + 4 * t, j = ins * 64 + lane, r = j / KPS, pc = j % KPS;
+    k_on[t] = ins < K_INS && pc < KPS - 1;
+    k_row[t] = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);     // key of LDS row r
+    k_col[t] = pc * 8;
+  }
 #pragma unroll
-    for (int i = 0; i < V_IT; ++i) {
-      const int c = min(tid + i * 256, V_CH - 1);
-      const int r = c / (AK / 8), col = (c % (AK / 8)) * 8;
-      rv[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)r * p.sk_pad + kv0 + col);
-    }
+  for (int t = 0; t < V_IW; ++t) {
+    const int ins = wave + 4 * t, j = ins * 64 + lane, r = j / VPS, pc = j % VPS;
+    v_on[t] = ins < V_INS && pc < VPS - 1 && r < D;
+    v_off[t] = r * p.sk_pad + pc * 8;
+  }
+  auto dma = [&](int kv0, bf16_t* kl, bf16_t* vl) {
+#pragma unroll
+    for (int t = 0; t < K_IW; ++t)
+      if (k_on[t]) attn_dma16(K + (size_t)min(kv0 + k_row[t], p.sk - 1) * p.k_row + k_col[t], kl + (wave + 4 * t) * 512);
+#pragma unroll
+    for (int t = 0; t < V_IW; ++t)
+      if (v_on[t]) attn_dma16(VT + v_off[t] + kv0, vl + (wave + 4 * t) * 512);
   };
-  auto vpos = [](int key) { const int bk = (key >> 2) & 3; return (key & ~15) + 4 * (((bk & 1) << 1) | (bk >> 1)); };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < K_IT; ++i) {
-      const int c = tid + i * 256;
-      if (c < K_CH) {
-        const int r = c / (D / 8), col = (c % (D / 8)) * 8;
-        *reinterpret_cast<u32x4*>(&ks[r * KP + col]) = rk[i];
-      }
+  if constexpr (ONES) {       // rows D .. DP-1 of both V^T stages: bf16 ones, never overwritten
+    for (int i = tid; i < (DP - D) * VP / 2; i += 256) {
+      reinterpret_cast<uint32_t*>(vs0 + D * VP)[i] = 0x3f803f80u;
+      reinterpret_cast<uint32_t*>(vs1 + D * VP)[i] = 0x3f803f80u;
     }
-#pragma unroll
-    for (int i = 0; i < V_IT; ++i) {
-      const int c = tid + i * 256;
-      if (c < V_CH) {
-        const int r = c / (AK / 8), col = (c % (AK / 8)) * 8;
-        *reinterpret_cast<uint2*>(&vs[r * VP + vpos(col)]) = make_uint2(rv[i][0], rv[i][1]);
-        *reinterpret_cast<uint2*>(&vs[r * VP + vpos(col + 4)]) = make_uint2(rv[i][2], rv[i][3]);
-      }
-    }
-  };
-  if constexpr (ONES) {       // rows D .. DP-1 of the V^T tile: bf16 ones, never overwritten
-    for (int i = tid; i < (DP - D) * VP / 2; i += 256)
-      reinterpret_cast<uint32_t*>(vs + D * VP)[i] = 0x3f803f80u;
   }
 
   f32x16 o[2][NC];
@@ -380,14 +386,7 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
   const float scale = 1.4426950408889634f / sqrtf((float)D);
 
-  load_tile(0);
-  for (int kv0 = 0; kv0 < p.sk; kv0 += AK) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kv0 + AK < p.sk) load_tile(kv0 + AK);
-    if (!active) continue;
-
+  auto tile = [&](int kv0, const bf16_t* ks, const bf16_t* vs) {
     // the online softmax advances 32 keys at a time: half the score registers, and the next
     // block's S^T MFMAs are independent of this block's exponentials
 #pragma unroll
@@ -399,12 +398,13 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
         sacc[0] = mfma32(ka, qh[0][s], sacc[0]);
         sacc[1] = mfma32(ka, qh[1][s], sacc[1]);
       }
+      // element r of a lane is key kv0 + 32 kb + 16 (r / 8) + 8 g + r % 8
       if (kv0 + kb * 32 + 32 > p.sk) {
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (kv0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3) >= p.sk) sacc[u][r] = -INFINITY;
+            if (kv0 + kb * 32 + 16 * (r >> 3) + 8 * g + (r & 7) >= p.sk) sacc[u][r] = -INFINITY;
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -448,6 +448,21 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
         }
       }
     }
+  };
+
+  dma(0, ks0, vs0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kv0 = 0; kv0 < p.sk; kv0 += 2 * AK) {
+    if (kv0 + AK < p.sk) dma(kv0 + AK, ks1, vs1);
+    if (active) tile(kv0, ks0, vs0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (kv0 + AK >= p.sk) break;
+    if (kv0 + 2 * AK < p.sk) dma(kv0 + 2 * AK, ks0, vs0);
+    if (active) tile(kv0 + AK, ks1, vs1);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
   }
 
 #pragma unroll
