@@ -119,8 +119,29 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x4 (&a
       bias[2] = bf2f((bf16_t)(bb.y & 0xffff)); bias[3] = bf2f((bf16_t)(bb.y >> 16));
     }
   }
+  // residual / position rows of block i (rows past M clamped): the next block's are loaded
+  // while this block goes through the scratch, so one load latency is exposed per tile
+  constexpr bool XIN = EPI == EPI_RESID || EPI == EPI_POS;
+  auto load_x = [&](int i, float4 (&x)[NP]) {
+#pragma unroll
+    for (int t = 0; t < NP; ++t) {
+      const int m = min(row0 + i * 16 + t * RPI + prow, p.M - 1);
+      if constexpr (EPI == EPI_RESID) {
+        x[t] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.out) + (size_t)m * p.ldo + n);
+      } else {
+        const uint2 pp = *reinterpret_cast<const uint2*>(p.pos + (size_t)(m % p.pos_rows) * p.N + n);
+        x[t] = float4{bf2f((bf16_t)(pp.x & 0xffff)), bf2f((bf16_t)(pp.x >> 16)),
+                      bf2f((bf16_t)(pp.y & 0xffff)), bf2f((bf16_t)(pp.y >> 16))};
+      }
+    }
+  };
+  float4 xb[2][XIN ? NP : 1];
+  if constexpr (XIN) load_x(0, xb[0]);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    if constexpr (XIN) {
+      if (i + 1 < TM) load_x(i + 1, xb[(i + 1) & 1]);
+    }
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -135,21 +156,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x4 (&a
       if constexpr (SW) u[t] = *reinterpret_cast<const float4*>(sc + row * SP + c + 8);
     }
     asm volatile("" ::: "memory");
-    // residual / position rows are read for every pass first (rows past M clamped), then stored
-    float4 x[NP];
-    if constexpr (EPI == EPI_RESID || EPI == EPI_POS) {
-#pragma unroll
-      for (int t = 0; t < NP; ++t) {
-        const int m = min(row0 + i * 16 + t * RPI + prow, p.M - 1);
-        if constexpr (EPI == EPI_RESID) {
-          x[t] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.out) + (size_t)m * p.ldo + n);
-        } else {
-          const uint2 pp = *reinterpret_cast<const uint2*>(p.pos + (size_t)(m % p.pos_rows) * p.N + n);
-          x[t] = float4{bf2f((bf16_t)(pp.x & 0xffff)), bf2f((bf16_t)(pp.x >> 16)),
-                        bf2f((bf16_t)(pp.y & 0xffff)), bf2f((bf16_t)(pp.y >> 16))};
-        }
-      }
-    }
+    const float4* x = xb[i & 1];
 #pragma unroll
     for (int t = 0; t < NP; ++t) {
       const int m = row0 + i * 16 + t * RPI + prow;
