@@ -68,9 +68,12 @@ struct GemvArgs {
   const bf16_t* gain_out = nullptr;
   void* aout = nullptr;
   int ldao = 0;
+  // compute units the launch's stream may use (its CU partition, or the whole GPU): the K split
+  // is chosen from it
+  int cus = 0;
 };
-int gemv_splits(int N, int K, int B, bool f32x);
-size_t gemv_partial_floats(int B, int N, int K, bool f32x);
+int gemv_splits(int N, int K, int B, bool f32x, int cus);
+size_t gemv_partial_floats(int B, int N, int K, bool f32x, int cus);
 template <typename TX, typename OT>
 hipError_t gemv(const GemvArgs& p, int epi, hipStream_t s);
 

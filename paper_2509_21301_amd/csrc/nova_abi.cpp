@@ -57,6 +57,19 @@ struct Global {
 };
 Global g;
 
+// Compute units a stream may use: its CU mask's when it is one of the partition streams, else the
+// whole GPU's.
+int stream_cus(hipStream_t s) {
+  std::lock_guard<std::mutex> lk(g.mu);
+  for (const auto& ms : g.mask_streams)
+    if (ms.second == s) {
+      int n = 0;
+      for (uint32_t w : ms.first) n += __builtin_popcount(w);
+      return n > 0 ? n : g.cus;
+    }
+  return g.cus;
+}
+
 hipEvent_t take_event() {
   std::lock_guard<std::mutex> lk(g.mu);
   if (!g.ev_free.empty()) {
@@ -606,11 +619,11 @@ DecodeBufs<T> decode_bufs(const nova_llm* m, int B, int max_ctx, void* base) {
   d.counters = w.take<unsigned>((size_t)2 * c.layers * (H / 64));
   size_t part = 0;
   const bool f32 = sizeof(T) == 4;
-  part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden, f32));
-  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, qd, f32));
-  part = std::max(part, nova::gemv_partial_floats(B, 2 * m->ip, c.hidden, f32));
-  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, m->ip, f32));
-  part = std::max(part, nova::gemv_partial_floats(B, c.vocab, c.hidden, f32));
+  part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden, f32, g.cus));
+  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, qd, f32, g.cus));
+  part = std::max(part, nova::gemv_partial_floats(B, 2 * m->ip, c.hidden, f32, g.cus));
+  part = std::max(part, nova::gemv_partial_floats(B, c.hidden, m->ip, f32, g.cus));
+  part = std::max(part, nova::gemv_partial_floats(B, c.vocab, c.hidden, f32, g.cus));
   d.part = w.take<float>(part);
   d.apart = w.take<float>(nova::dec_attn_partial_floats(B, c.n_q, c.head_dim, max_ctx, c.n_kv));
   d.used = w.used;
@@ -646,6 +659,7 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
   const size_t split_floats = prefill_split_floats(m, S);
   float* split_ws = w.take<float>(split_floats);
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
+  const int cus = stream_cus(s);
   // the QKV, O and down projections may split K when their tiles cannot fill the GPU
   auto with_split = [&](GemmArgs p) {
     p.split_ws = split_ws;
@@ -688,6 +702,7 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
                                                  (const bf16_t*)(hw + m->head.off[0]), c.eps, a, H, keys, s));
   {
     GemvArgs p{a, H, (const bf16_t*)(hw + m->head.off[1]), H, 1, c.vocab, H, logits_out, c.vocab, nullptr, keys};
+    p.cus = cus;
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
   CALL(NOVA_KIND_MISC, s, nova::argmax_finish(keys, 1, next_id, s));
@@ -703,7 +718,8 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
   const bool f32 = sizeof(T) == 4;
   const int tiles = H / 64;
-  const int sp_qkv = nova::gemv_splits(m->qkvw, H, B, f32);
+  const int cus = stream_cus(s);
+  const int sp_qkv = nova::gemv_splits(m->qkvw, H, B, f32, cus);
   const char* hw = (const char*)m->d.head;
   auto layer_w = [&](int l, int i) {
     return (const bf16_t*)((const char*)m->d.layers + (size_t)l * m->lay.bytes + m->lay.off[i]);
@@ -733,36 +749,41 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
       auto W = [&](int i) { return layer_w(l, i); };
       {
         GemvArgs p{d.a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : d.qkv, m->qkvw, d.part, nullptr};
+        p.cus = cus;
         p.ss_in = ss(2 * l), p.ss_parts = tiles, p.eps = c.eps;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
       }
       if (const int rc = attention_block(l)) return rc;
       {
         GemvArgs p{d.att, qd, W(2), qd, B, H, qd, d.x, H, d.part, nullptr};
+        p.cus = cus;
         p.ss_out = ss(2 * l + 1), p.counters = d.counters + (size_t)(2 * l) * tiles;
         p.gain_out = W(3), p.aout = d.a, p.ldao = H;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
       }
       {
         GemvArgs p{d.a, H, W(4), H, B, 2 * m->ip, H, d.hm, m->ip, d.part, nullptr};
+        p.cus = cus;
         p.ss_in = ss(2 * l + 1), p.ss_parts = tiles, p.eps = c.eps;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
       }
       {
         GemvArgs p{d.hm, m->ip, W(5), m->ip, B, H, m->ip, d.x, H, d.part, nullptr};
+        p.cus = cus;
         p.ss_out = ss(2 * l + 2), p.counters = d.counters + (size_t)(2 * l + 1) * tiles;
         p.gain_out = l + 1 < c.layers ? layer_w(l + 1, 0) : final_gain, p.aout = d.a, p.ldao = H;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
       }
     }
     GemvArgs p{d.a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, d.part, d.keys};
+    p.cus = cus;
     p.ss_in = ss(2 * c.layers), p.ss_parts = tiles, p.eps = c.eps;
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   } else {
     // Larger batches: a residual + RMSNorm kernel sums the O / down split-K partials into x and
     // writes the normalised rows for the next projection.
-    const int sp_o = nova::gemv_splits(H, qd, B, f32);
-    const int sp_down = nova::gemv_splits(H, m->ip, B, f32);
+    const int sp_o = nova::gemv_splits(H, qd, B, f32, cus);
+    const int sp_down = nova::gemv_splits(H, m->ip, B, f32, cus);
     CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(nullptr, 0, ids, B, (const bf16_t*)m->d.embed, H, d.x, s));
     CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, d.x, B, H, c.layers > 0 ? layer_w(0, 0) : final_gain, c.eps,
                                                    d.a, H, c.layers > 0 ? nullptr : d.keys, s));
@@ -770,21 +791,25 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
       auto W = [&](int i) { return layer_w(l, i); };
       {
         GemvArgs p{d.a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : d.qkv, m->qkvw, d.part, nullptr};
+        p.cus = cus;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
       }
       if (const int rc = attention_block(l)) return rc;
       {
         GemvArgs p{d.att, qd, W(2), qd, B, H, qd, sp_o > 1 ? nullptr : d.x, H, d.part, nullptr};
+        p.cus = cus;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
       }
       CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_o > 1 ? d.part : nullptr, sp_o > 1 ? sp_o : 0, d.x, B, H, W(3), c.eps,
                                                      d.a, H, nullptr, s));
       {
         GemvArgs p{d.a, H, W(4), H, B, 2 * m->ip, H, d.hm, m->ip, d.part, nullptr};
+        p.cus = cus;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
       }
       {
         GemvArgs p{d.hm, m->ip, W(5), m->ip, B, H, m->ip, sp_down > 1 ? nullptr : d.x, H, d.part, nullptr};
+        p.cus = cus;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
       }
       CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_down > 1 ? d.part : nullptr, sp_down > 1 ? sp_down : 0, d.x, B, H,
@@ -792,6 +817,7 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
                                                      l + 1 < c.layers ? nullptr : d.keys, s));
     }
     GemvArgs p{d.a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, d.part, d.keys};
+    p.cus = cus;
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
   CALL(NOVA_KIND_MISC, s, nova::argmax_finish(d.keys, B, next_ids, s));

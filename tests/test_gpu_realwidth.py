@@ -10,7 +10,7 @@ one by one (through the C ABI, bf16, tolerance 2e-2):
 * decode: 4 and 20 sequences with ragged contexts of 1200..1500 tokens in a shuffled paged cache
   (random bf16 K/V shared with the oracle) -- logits of every sequence and the appended K/V; the
   small batch runs the step with its RMSNorms folded into the projections, the large one with
-  separate residual + norm kernels.
+  separate residual + norm kernels; each on the whole GPU and on a 64-CU partition.
 """
 import dataclasses
 
@@ -95,8 +95,10 @@ def test_prefill_layer_real_width(gpu_lib, llm1):
         assert vlm.max_rel_err(v5[0, blk, :, :, slot], v[p]) < sc.TOL_BF16
 
 
-@pytest.mark.parametrize("bsz", [4, 20])
-def test_decode_real_width(gpu_lib, llm1, bsz):
+# the thin GEMMs split K by the stream's CU count: on a 64-CU partition the O and down
+# projections run unsplit, the residual update and the folded norm in the direct epilogue
+@pytest.mark.parametrize("bsz,cus", [(4, None), (20, None), (4, 64), (20, 64)])
+def test_decode_real_width(gpu_lib, llm1, bsz, cus):
     import torch
     nova = gpu_lib
     w, llm = llm1
@@ -113,8 +115,10 @@ def test_decode_real_width(gpu_lib, llm1, bsz):
     ids = synth.text_ids(bsz, cfg.vocab, seed=12)
     pos = np.array(ctx, np.int32)
     logits = torch.empty(bsz, cfg.vocab, dtype=torch.float32, device="cuda")
-    nxt = llm.decode(torch.from_numpy(ids).cuda(), torch.from_numpy(pos).cuda(), torch.from_numpy(tables).cuda(),
-                     kv, max_ctx=max(ctx) + 1, logits=logits)
+    stream = None if cus is None else nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(cus, 0))
+    args = (torch.from_numpy(ids).cuda(), torch.from_numpy(pos).cuda(), torch.from_numpy(tables).cuda())
+    torch.cuda.synchronize()
+    nxt = llm.decode(*args, kv, max_ctx=max(ctx) + 1, logits=logits, stream=stream)
     torch.cuda.synchronize()
     ref_logits, ref_ids = vlm.llm_decode_step(ids, pos, tables, kref, w, cfg)
     got = logits.cpu().numpy()
