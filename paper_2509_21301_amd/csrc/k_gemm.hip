@@ -521,6 +521,16 @@ static int split_slices(const GemmArgs& p) {
   return best;
 }
 
+// The output pointer moved by (rows, cols) elements: the residual and position epilogues write
+// fp32 whatever OT is.
+template <typename OT, int EPI>
+static void* out_at(const GemmArgs& p, size_t rows, size_t cols) {
+  if constexpr (EPI == EPI_RESID || EPI == EPI_POS)
+    return reinterpret_cast<float*>(p.out) + rows * p.ldo + cols;
+  else
+    return reinterpret_cast<OT*>(p.out) + rows * p.ldo + cols;
+}
+
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when there are at least two tiles per
@@ -564,7 +574,23 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         b.N = p.N - n1;
         b.W = p.W + (size_t)n1 * p.ldw;
         if (p.bias) b.bias = p.bias + n1;
-        b.out = reinterpret_cast<OT*>(p.out) + (EPI == EPI_SWIGLU ? n1 / 2 : n1);
+        b.out = out_at<OT, EPI>(p, 0, EPI == EPI_SWIGLU ? n1 / 2 : n1);
+        return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
+      }
+      // many row tiles and a long K with a last round of 256x256 tiles mostly idle (the ViT's MLP
+      // down projection at 8 images: 810 tiles, K = 5120): the rows of whole rounds as 256x256
+      // tiles, the remaining rows as 128x128 tiles, which fit the GPU in one round
+      const int m_tiles1 = (int)(rounds * 256 / (p.N / 256));
+      if (p.K >= 4096 && tiles % 256 != 0 && tiles % 256 < 64 && m_tiles1 > 16 && m_tiles1 < nm && EPI != EPI_POS &&
+          p.vt == nullptr) {
+        GemmArgs a = p;
+        a.M = m_tiles1 * 256;
+        hipError_t e = launch_dma<OT, EPI, 256, 256, 64, 128>(a, s);
+        if (e != hipSuccess) return e;
+        GemmArgs b = p;
+        b.M = p.M - a.M;
+        b.A = reinterpret_cast<const bf16_t*>(p.A) + (size_t)a.M * p.lda;
+        b.out = out_at<OT, EPI>(p, a.M, 0);
         return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
       }
       return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
