@@ -538,6 +538,11 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   // when those tiles cannot fill the GPU (and the caller gave a workspace).
   if constexpr (sizeof(TA) == 2 && (EPI == EPI_STORE || EPI == EPI_RESID)) {
     const long tiles256 = (long)((p.M + 255) / 256) * (p.N / 256);
+    // a very long K whose 256x256 tiles make one round of at least three quarters of the GPU
+    // (the 3.6k-token prefill's down projection: 14 x 14 tiles, K = 18944): one unsplit launch,
+    // without the split partials' traffic
+    if (p.N % 256 == 0 && p.K >= 8192 && tiles256 >= 192 && tiles256 <= 256)
+      return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     if (!(p.N % 256 == 0 && tiles256 >= 512)) {
       const int sl = split_slices(p);
       if (sl > 1) {
