@@ -108,7 +108,8 @@ def decode_bytes(cfg, batch, ctx):
 
 # ----------------------------------------------------------------------------- HBM traffic
 def gemm_traffic():
-    """HBM bytes per GEMM launch of the encode pass, from the committed rocprofv3 PMC summary
+    """HBM bytes per GEMM call of the encode pass (one call of the GEMM routine, the unit timed
+    below; the split problems launch two kernels per call), from the committed rocprofv3 PMC summary
     (FETCH_SIZE and WRITE_SIZE, each scaled by its reading for a plain 1 GiB copy); None when the
     summary is missing or the GEMM source has changed since the counters were taken."""
     import hashlib
