@@ -6,7 +6,8 @@ one by one (through the C ABI, bf16, tolerance 2e-2):
   2-layer encoder with the same head size over 200 patches (a ragged last key tile) -- every
   merged token;
 * prefill: one 3584-wide GQA layer (28/4 heads of 128, SwiGLU 18944, vocab 152064) over
-  1300 visual embeddings + 200 text tokens -- last-row logits, greedy id, sampled K/V;
+  1300 visual embeddings + 200 text tokens, and over a screenshot's 3354 + 225 -- last-row logits,
+  greedy id, sampled K/V;
 * decode: 4 and 20 sequences with ragged contexts of 1200..1500 tokens in a shuffled paged cache
   (random bf16 K/V shared with the oracle) -- logits of every sequence and the appended K/V; the
   small batch runs the step with its RMSNorms folded into the projections, the large one with
@@ -64,11 +65,13 @@ def llm1():
     return w, nova.Llm(LLM1, w)
 
 
-def test_prefill_layer_real_width(gpu_lib, llm1):
+# 1500 tokens (the benchmark's prompt) and 3579 (a 1092x2408 screenshot's 3354 visual tokens and 225
+# text tokens, the serving prompt), whose MLP down projection runs as one unsplit 256x256 launch
+@pytest.mark.parametrize("nv,nt", [(synth.LLM_VISION_TOKENS, synth.LLM_TEXT_TOKENS), (3354, 225)])
+def test_prefill_layer_real_width(gpu_lib, llm1, nv, nt):
     import torch
     nova = gpu_lib
     w, llm = llm1
-    nv, nt = synth.LLM_VISION_TOKENS, synth.LLM_TEXT_TOKENS
     vis = synth.vision_embeds(nv, LLM1.hidden)
     ids = synth.text_ids(nt, LLM1.vocab)
     s = nv + nt
@@ -79,7 +82,7 @@ def test_prefill_layer_real_width(gpu_lib, llm1):
                       torch.from_numpy(table[0]).cuda(), kv, logits=logits)
     torch.cuda.synchronize()
     x = np.concatenate([vis, w["embed"][ids]], 0)
-    rows = np.array([0, 777, 1299, 1300, s - 1])
+    rows = np.array(sorted({0, 777, nv - 1, nv, s - 80, s - 1}))
     hid, k, v = vlm.llm_layer_rows(x, w, 0, LLM1, rows)
     ref_logits = vlm.lm_head(hid[-1:], w, LLM1)[0]
     got = logits.cpu().numpy()
@@ -89,7 +92,7 @@ def test_prefill_layer_real_width(gpu_lib, llm1):
         assert int(nxt.item()) == int(np.argmax(ref_logits))
     k5 = kv.k5.float().cpu().numpy()
     v5 = kv.v5.float().cpu().numpy()
-    for p in [0, 15, 16, 1000, s - 1]:
+    for p in [0, 15, 16, 1000, s - 80, s - 1]:
         blk, slot = table[0][p // 16], p % 16
         assert vlm.max_rel_err(k5[0, blk, :, slot, :], k[p]) < sc.TOL_BF16
         assert vlm.max_rel_err(v5[0, blk, :, :, slot], v[p]) < sc.TOL_BF16
