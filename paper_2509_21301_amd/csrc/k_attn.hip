@@ -296,6 +296,54 @@ __device__ __forceinline__ void attn_dma16(const bf16_t* g, bf16_t* l_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l_base, 16, 0, 0);
 }
 
+// Light-block sweep of attn_wide_kernel: one 32-key step of one query group.  Row i of the score
+// accumulator holds key perm(i) (the middle 4-row blocks of each 16 swapped, as in the LDS tiles),
+// so a lane's probabilities of chunk tt are keys 16 tt + 8 g .. + 7 in order.
+template <int D, int NS, int NC, bool ONES>
+__device__ __forceinline__ void light_step(const Frag8 (&q1)[NS], const Frag8 (&kf)[NS], const Frag8 (&vf)[2][NC],
+                                           int key0, int sk, int g, float scale, f32x16 (&o1)[NC], float& m1,
+                                           float& l1) {
+  f32x16 sacc = f32x16{};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) sacc = mfma32(kf[s], q1[s], sacc);
+  if (key0 + 32 > sk) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (key0 + 16 * (r >> 3) + 8 * g + (r & 7) >= sk) sacc[r] = -INFINITY;
+  }
+  float tmax = -1e30f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[r]);
+  tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+  const float m_new = fmaxf(m1, tmax);
+  const float ms = m_new * scale;
+  float rsum = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[r], scale, -ms));
+    sacc[r] = pv;
+    if constexpr (!ONES) rsum += pv;
+  }
+  if (__ballot(m_new > m1)) {
+    const float corr = __builtin_amdgcn_exp2f((m1 - m_new) * scale);
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o1[c][r] *= corr;
+    if constexpr (!ONES) l1 *= corr;
+  }
+  if constexpr (!ONES) l1 += rsum + __shfl_xor(rsum, 32, 64);
+  m1 = m_new;
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    Frag8 ph;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ph.w[e] = pack2(sacc[8 * tt + 2 * e], sacc[8 * tt + 2 * e + 1]);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) o1[c] = mfma32(vf[tt][c], ph, o1[c]);
+  }
+}
+
 template <int D>
 __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   constexpr int NS = D / 16;
@@ -314,17 +362,32 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, lq = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // scalar: uniform branches
   const int nqb = (p.sq + AQW - 1) / AQW;
+  // A last query block of at most 64 queries ("light") would keep three of its four waves idle
+  // for a whole key sweep and, with every other block full, add a round of workgroups at the end
+  // (8 images of 5184 patches: 20 full blocks and one of 64 queries per head).  Light blocks are
+  // dispatched first; each of their waves takes one query group and one 32-key half of every tile.
+  const bool has_light = p.sq % AQW != 0 && p.sq % AQW <= 64;
+  const int pairs = p.batch * p.n_q;
   int qb, h, b;
+  bool light = false;
   {
-    const int pairs = p.batch * p.n_q, lin = blockIdx.x;
+    const int lin = blockIdx.x;
     int pair;
-    if (pairs % 8 == 0) {
-      const int j = lin >> 3;
-      pair = (lin & 7) * (pairs >> 3) + j / nqb;
-      qb = j % nqb;
+    if (has_light && lin < pairs) {
+      light = true;
+      qb = nqb - 1;
+      // a pair's light block on the XCD of its full blocks (same L2)
+      pair = pairs % 8 == 0 ? (lin & 7) * (pairs >> 3) + (lin >> 3) : lin;
     } else {
-      pair = lin / nqb;
-      qb = lin % nqb;
+      const int lin2 = lin - (has_light ? pairs : 0), nfull = has_light ? nqb - 1 : nqb;
+      if (pairs % 8 == 0) {
+        const int j = lin2 >> 3;
+        pair = (lin2 & 7) * (pairs >> 3) + j / nfull;
+        qb = j % nfull;
+      } else {
+        pair = lin2 / nfull;
+        qb = lin2 % nfull;
+      }
     }
     h = pair % p.n_q;
     b = pair / p.n_q;
@@ -337,15 +400,7 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   const bf16_t* K = reinterpret_cast<const bf16_t*>(p.k) + (size_t)b * p.k_batch + (size_t)kvh * D;
   const bf16_t* VT = reinterpret_cast<const bf16_t*>(p.vt) + ((size_t)b * p.n_kv + kvh) * D * (size_t)p.sk_pad;
 
-  Frag8 qh[2][NS];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int qrow = qbase + 32 * u + lq;
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      qh[u][s] = qrow < p.sq ? *reinterpret_cast<const Frag8*>(Q + (size_t)qrow * p.q_row + 16 * s + 8 * g) : zero_frag();
-  }
-
+  const float scale = 1.4426950408889634f / sqrtf((float)D);
   // DMA instruction i (dealt to wave i % 4) fills LDS slots 64 i .. 64 i + 63 of a tile, slot j
   // being piece j % (slots per row) of LDS row j / (slots per row); pad slots are masked off
   int k_row[K_IW], k_col[K_IW], v_off[V_IW];
@@ -378,13 +433,98 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
     }
   }
 
+  if (light) {
+    // wave w: key half w & 1 of every 64-key tile and query group w >> 1 of the block's 64 queries;
+    // K and V^T tiles come through the same double-buffered DMA stages as for a full block, each
+    // wave doing a quarter of a full wave's MFMAs per tile.  The two key halves of a query group
+    // are merged through LDS at the end.
+    const int kb = wave & 1, u = wave >> 1;
+    const int qrow = qb * AQW + 32 * u + lq;
+    const bool lact = qb * AQW + 32 * u < p.sq;
+    Frag8 q1[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      q1[s] = qrow < p.sq ? *reinterpret_cast<const Frag8*>(Q + (size_t)qrow * p.q_row + 16 * s + 8 * g) : zero_frag();
+    f32x16 o1[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) o1[c] = f32x16{};
+    float m1 = -1e30f, l1 = 0.f;
+    auto ltile = [&](int kv0, const bf16_t* ks, const bf16_t* vs) {
+      Frag8 kf[NS], vf[2][NC];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) kf[s] = *reinterpret_cast<const Frag8*>(&ks[(kb * 32 + lq) * KP + 16 * s + 8 * g]);
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          vf[tt][c] = *reinterpret_cast<const Frag8*>(&vs[(c * 32 + lq) * VP + kb * 32 + 16 * tt + 8 * g]);
+      light_step<D, NS, NC, ONES>(q1, kf, vf, kv0 + 32 * kb, p.sk, g, scale, o1, m1, l1);
+    };
+    dma(0, ks0, vs0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int kv0 = 0; kv0 < p.sk; kv0 += 2 * AK) {
+      if (kv0 + AK < p.sk) dma(kv0 + AK, ks1, vs1);
+      if (lact) ltile(kv0, ks0, vs0);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (kv0 + AK >= p.sk) break;
+      if (kv0 + 2 * AK < p.sk) dma(kv0 + 2 * AK, ks0, vs0);
+      if (lact) ltile(kv0 + AK, ks1, vs1);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+    // the second-half wave of group u leaves (o, m, l) in V^T stage u (every tile read is done),
+    // the first-half wave combines them and writes the output
+    constexpr int CW = NC * 16 + 2;                     // floats per lane
+    static_assert((size_t)CW * 64 * 4 <= sizeof(vs0), "merge buffer");
+    float* cb = reinterpret_cast<float*>(u ? vs1 : vs0);
+    if (kb) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cb[(c * 16 + r) * 64 + lane] = o1[c][r];
+      cb[(NC * 16) * 64 + lane] = m1;
+      cb[(NC * 16 + 1) * 64 + lane] = l1;
+    }
+    __syncthreads();
+    if (kb || qrow >= p.sq) return;
+    const float m2 = cb[(NC * 16) * 64 + lane], l2 = cb[(NC * 16 + 1) * 64 + lane];
+    const float mm = fmaxf(m1, m2);
+    const float f1 = __builtin_amdgcn_exp2f((m1 - mm) * scale), f2 = __builtin_amdgcn_exp2f((m2 - mm) * scale);
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o1[c][r] = o1[c][r] * f1 + cb[(c * 16 + r) * 64 + lane] * f2;
+    const float inv = 1.0f / (ONES ? o1[NC - 1][8] : l1 * f1 + l2 * f2);
+    bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + (size_t)b * p.o_batch + (size_t)qrow * p.o_row + (size_t)h * D;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + 8 * r4 + 4 * g;
+        if (col >= D) continue;
+        *reinterpret_cast<uint2*>(out + col) =
+            make_uint2(pack2(o1[c][4 * r4] * inv, o1[c][4 * r4 + 1] * inv), pack2(o1[c][4 * r4 + 2] * inv, o1[c][4 * r4 + 3] * inv));
+      }
+    return;
+  }
+
+  Frag8 qh[2][NS];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int qrow = qbase + 32 * u + lq;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qh[u][s] = qrow < p.sq ? *reinterpret_cast<const Frag8*>(Q + (size_t)qrow * p.q_row + 16 * s + 8 * g) : zero_frag();
+  }
+
   f32x16 o[2][NC];
 #pragma unroll
   for (int u = 0; u < 2; ++u)
 #pragma unroll
     for (int c = 0; c < NC; ++c) o[u][c] = f32x16{};
   float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
-  const float scale = 1.4426950408889634f / sqrtf((float)D);
 
   auto tile = [&](int kv0, const bf16_t* ks, const bf16_t* vs) {
     // the online softmax advances 32 keys at a time: half the score registers, and the next
