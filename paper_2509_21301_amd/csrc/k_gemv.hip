@@ -308,21 +308,30 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
       float* xo = reinterpret_cast<float*>(p.out);
       const int n0 = blockIdx.x * GV_ROWS;
       const float gn = p.gain_out != nullptr ? bf2f(p.gain_out[n0 + lane]) : 0.f;
-      // wave w takes batch rows w, w + 4, ... (at most 8); lane = row within the tile; all of a
-      // split's loads are issued before any is summed
+      // wave w takes batch rows w, w + 4, ... (at most 8); lane = row within the tile.  Each load is
+      // a round trip to the coherent level, so the loads of 8 splits are all issued before any is
+      // summed (then summed in split order)
       constexpr int BPW = (16 * NB + 3) / 4;
       float v[BPW];
 #pragma unroll
       for (int i = 0; i < BPW; ++i) v[i] = 0.f;
-#pragma unroll 4
-      for (int sp = 0; sp < (int)gridDim.y; ++sp) {
+      for (int sp0 = 0; sp0 < (int)gridDim.y; sp0 += 8) {
+        float t[8][BPW];
 #pragma unroll
-        for (int i = 0; i < BPW; ++i) {
-          const int b = wave + 4 * i;
-          if (b < p.B)
-            v[i] += __hip_atomic_load(p.partial + ((size_t)sp * p.B + b) * p.N + n0 + lane, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
-        }
+        for (int k = 0; k < 8; ++k)
+#pragma unroll
+          for (int i = 0; i < BPW; ++i) {
+            const int b = wave + 4 * i, sp = sp0 + k;
+            t[k][i] = b < p.B && sp < (int)gridDim.y
+                          ? __hip_atomic_load(p.partial + ((size_t)sp * p.B + b) * p.N + n0 + lane, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT)
+                          : 0.f;
+          }
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+#pragma unroll
+          for (int i = 0; i < BPW; ++i)
+            if (sp0 + k < (int)gridDim.y) v[i] += t[k][i];
       }
 #pragma unroll
       for (int i = 0; i < BPW; ++i) {
