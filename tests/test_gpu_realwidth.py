@@ -3,8 +3,8 @@ one by one (through the C ABI, bf16, tolerance 2e-2):
 
 * vision encode: one 1280-wide layer (16 heads of 80, MLP 5120) on two 1008x1008 images
   (5184 patches each) with the 2x2 merge to 3584 -- sampled merged tokens of both images; and a
-  2-layer encoder with the same head size over 200 patches (a ragged last key tile) -- every
-  merged token;
+  2-layer encoder with the same head size over 200 patches (a ragged last key tile) and over 288
+  and 300 patches (a last query block of 32 and 44 queries) -- every merged token;
 * prefill: one 3584-wide GQA layer (28/4 heads of 128, SwiGLU 18944, vocab 152064) over
   1300 visual embeddings + 200 text tokens, and over a screenshot's 3354 + 225 -- last-row logits,
   greedy id, sampled K/V;
@@ -46,14 +46,22 @@ VIT_D80 = synth.VitConfig(hidden=640, heads=8, mlp=1280, layers=2, patch=14, mer
                           image_h=140, image_w=280, name="vit2_d80_ragged")
 
 
-def test_vit_head80_ragged_keys(gpu_lib):
+# The same encoder over 16x18 and 10x30 grids: 288 and 300 patches leave a last query block of 32
+# and of 44 queries, which runs as a light block (one query group and one 32-key half of every tile
+# per wave, halves merged at the end): with the second query group empty, and half filled.
+VIT_D80_LIGHT32 = dataclasses.replace(VIT_D80, image_h=224, image_w=252, name="vit2_d80_light32")
+VIT_D80_LIGHT44 = dataclasses.replace(VIT_D80, image_h=140, image_w=420, name="vit2_d80_light44")
+
+
+@pytest.mark.parametrize("cfg", [VIT_D80, VIT_D80_LIGHT32, VIT_D80_LIGHT44], ids=lambda c: c.name)
+def test_vit_head80_ragged_keys(gpu_lib, cfg):
     import torch
     nova = gpu_lib
-    w = synth.vit_weights(VIT_D80, seed=4)
-    imgs = synth.image(2, VIT_D80.image_h, VIT_D80.image_w, seed=6)
-    out = nova.Vit(VIT_D80, w).encode(torch.from_numpy(imgs).cuda().to(torch.bfloat16)).float().cpu().numpy()
+    w = synth.vit_weights(cfg, seed=4)
+    imgs = synth.image(2, cfg.image_h, cfg.image_w, seed=6)
+    out = nova.Vit(cfg, w).encode(torch.from_numpy(imgs).cuda().to(torch.bfloat16)).float().cpu().numpy()
     for i in range(2):
-        ref = vlm.vit_encode(imgs[i], w, VIT_D80)
+        ref = vlm.vit_encode(imgs[i], w, cfg)
         assert vlm.max_rel_err(out[i], ref) < sc.TOL_BF16, f"image {i}"
 
 
