@@ -25,6 +25,19 @@ namespace nova {
 constexpr int AQ = 128;   // queries per workgroup
 constexpr int AK = 64;    // keys per tile
 
+// Combine a value with that of lane ^ 32 (the other half of the wavefront holds the same query
+// columns of a 32x32 MFMA tile): gfx950's permlane32 swap exchanges the two halves in the VALU,
+// without the LDS round trip of a general shuffle.  Swapping x with itself gives, in every lane,
+// x of that lane and of its partner.
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <typename T, int D, bool CAUSAL>
 __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   constexpr bool F32 = sizeof(T) == 4;
@@ -205,7 +218,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[kb][r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    tmax = max_halves(tmax);
     const float m_new = fmaxf(m_run, tmax);
     const float ms = m_new * scale;
     float rsum = 0.f;
@@ -217,7 +230,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
         sacc[kb][r] = pv;
         rsum += pv;
       }
-    rsum += __shfl_xor(rsum, 32, 64);
+    rsum = sum_halves(rsum);
     if (__ballot(m_new > m_run)) {       // rescale only when some query's max moved
       const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * scale);
       l_run *= corr;
@@ -314,7 +327,7 @@ __device__ __forceinline__ void light_step(const Frag8 (&q1)[NS], const Frag8 (&
   float tmax = -1e30f;
 #pragma unroll
   for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[r]);
-  tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+  tmax = max_halves(tmax);
   const float m_new = fmaxf(m1, tmax);
   const float ms = m_new * scale;
   float rsum = 0.f;
@@ -332,7 +345,7 @@ __device__ __forceinline__ void light_step(const Frag8 (&q1)[NS], const Frag8 (&
       for (int r = 0; r < 16; ++r) o1[c][r] *= corr;
     if constexpr (!ONES) l1 *= corr;
   }
-  if constexpr (!ONES) l1 += rsum + __shfl_xor(rsum, 32, 64);
+  if constexpr (!ONES) l1 += sum_halves(rsum);
   m1 = m_new;
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
@@ -551,7 +564,7 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
         float tmax = -1e30f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[u][r]);
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        tmax = max_halves(tmax);
         const float m_new = fmaxf(m_run[u], tmax);
         const float ms = m_new * scale;
         float rsum = 0.f;
@@ -569,7 +582,7 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
             for (int r = 0; r < 16; ++r) o[u][c][r] *= corr;
           if constexpr (!ONES) l_run[u] *= corr;
         }
-        if constexpr (!ONES) l_run[u] += rsum + __shfl_xor(rsum, 32, 64);
+        if constexpr (!ONES) l_run[u] += sum_halves(rsum);
         m_run[u] = m_new;
       }
 #pragma unroll
