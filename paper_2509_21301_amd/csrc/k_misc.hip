@@ -337,6 +337,54 @@ hipError_t resid_rmsnorm(const float* partial, int splits, float* x, int B, int 
   return hipGetLastError();
 }
 
+// Decode residual fold for larger batches, spread over the whole GPU: workgroup (t, r) takes
+// columns 64t .. 64t+63 of rows 8r .. 8r+7, one 32-lane half-wave per row and two columns per
+// lane.  x[b] += sum_s partial[s][b] (if splits > 0), a[b] = x[b] * g, and the tile's sum of
+// squares of x[b] goes to ss_out[t * B + b]; the normalising consumer sums the H / 64 tile parts
+// and scales its outputs by the row's rsqrt.
+template <typename T>
+__global__ void __launch_bounds__(256) resid_fold_kernel(const float* __restrict__ partial, int splits,
+                                                         float* __restrict__ x, int B, int H,
+                                                         const bf16_t* __restrict__ g, T* __restrict__ a, int lda,
+                                                         float* __restrict__ ss_out) {
+  const int t = threadIdx.x, b = blockIdx.y * 8 + (t >> 5);
+  const int c = blockIdx.x * 64 + (t & 31) * 2;
+  float sq = 0.f;
+  if (b < B) {
+    float* xp = x + (size_t)b * H + c;
+    float2 v = *reinterpret_cast<const float2*>(xp);
+    if (splits > 0) {
+      float2 acc = make_float2(0.f, 0.f);
+#pragma unroll 8
+      for (int sp = 0; sp < splits; ++sp) {
+        const float2 pv = *reinterpret_cast<const float2*>(partial + ((size_t)sp * B + b) * H + c);
+        acc.x += pv.x;
+        acc.y += pv.y;
+      }
+      v.x += acc.x;
+      v.y += acc.y;
+      *reinterpret_cast<float2*>(xp) = v;
+    }
+    sq = v.x * v.x + v.y * v.y;
+    T* ap = a + (size_t)b * lda + c;
+    ap[0] = from_f<T>(v.x * bf2f(g[c]));
+    ap[1] = from_f<T>(v.y * bf2f(g[c + 1]));
+  }
+#pragma unroll
+  for (int o = 16; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+  if ((t & 31) == 0 && b < B) ss_out[(size_t)blockIdx.x * B + b] = sq;
+}
+
+template <typename T>
+hipError_t resid_fold(const float* partial, int splits, float* x, int B, int H, const bf16_t* g, T* a, int lda,
+                      float* ss_out, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (H % 64 || lda % 2 || (splits > 0 && !partial) || !ss_out) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((resid_fold_kernel<T>), dim3(H / 64, (B + 7) / 8), dim3(256), 0, s, partial, splits, x, B, H, g, a,
+                     lda, ss_out);
+  return hipGetLastError();
+}
+
 __global__ void argmax_finish_kernel(const unsigned long long* __restrict__ keys, int B, int* __restrict__ ids) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b < B) ids[b] = (int)~(uint32_t)(keys[b] & 0xffffffffull);
@@ -496,6 +544,9 @@ template hipError_t qkv_decode<bf16_t>(const float*, int, int, int, int, int, fl
 template hipError_t qkv_decode<float>(const float*, int, int, int, int, int, float, const int*, float*, float*, float*, const int*, int, int, hipStream_t);
 template hipError_t resid_rmsnorm<bf16_t>(const float*, int, float*, int, int, const bf16_t*, float, bf16_t*, int, unsigned long long*, hipStream_t);
 template hipError_t resid_rmsnorm<float>(const float*, int, float*, int, int, const bf16_t*, float, float*, int, unsigned long long*, hipStream_t);
+template hipError_t resid_fold<bf16_t>(const float*, int, float*, int, int, const bf16_t*, bf16_t*, int, float*,
+                                       hipStream_t);
+template hipError_t resid_fold<float>(const float*, int, float*, int, int, const bf16_t*, float*, int, float*, hipStream_t);
 template hipError_t embed_rows<bf16_t>(const bf16_t*, int, const int*, int, const bf16_t*, int, float*, hipStream_t);
 template hipError_t embed_rows<float>(const float*, int, const int*, int, const bf16_t*, int, float*, hipStream_t);
 

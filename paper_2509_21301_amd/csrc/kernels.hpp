@@ -138,6 +138,12 @@ hipError_t qkv_decode(const float* qkv, int splits, int B, int n_q, int n_kv, in
 template <typename T>
 hipError_t resid_rmsnorm(const float* partial, int splits, float* x, int B, int H, const bf16_t* g, float eps, T* a,
                          int lda, unsigned long long* keys, hipStream_t s);
+// Decode residual fold, column tiles of 64 over the whole GPU (H % 64 == 0): x[b] += sum_s
+// partial[s][b] (if splits > 0), a[b] = x[b] * g, ss_out[t * B + b] = sum of squares of tile t of
+// x[b], for a consumer that normalises from the H / 64 tile parts.
+template <typename T>
+hipError_t resid_fold(const float* partial, int splits, float* x, int B, int H, const bf16_t* g, T* a, int lda,
+                      float* ss_out, hipStream_t s);
 // ids[b] = the token id packed in keys[b] by the fused argmax.
 hipError_t argmax_finish(const unsigned long long* keys, int B, int* ids, hipStream_t s);
 // x[r] = r < n_vis ? vis[r] : embed[ids[r - n_vis]]  (fp32 out)

@@ -192,6 +192,7 @@ int check_llm_cfg(const nova_llm_config* c) {
   if (c->n_q / c->n_kv > 16) return fail(NOVA_EUNSUPPORTED, "at most 16 query heads per KV head");
   if (c->hidden % 256 || (c->n_q * c->head_dim) % 256 || c->vocab % 128)
     return fail(NOVA_EUNSUPPORTED, "hidden and n_q*head_dim must be multiples of 256, vocab of 128");
+  if (c->hidden > 4096) return fail(NOVA_EUNSUPPORTED, "hidden %d above 4096 (decode normalises from at most 64 column tiles)", c->hidden);
   if (((c->n_q + 2 * c->n_kv) * c->head_dim) % 128) return fail(NOVA_EUNSUPPORTED, "(n_q+2n_kv)*head_dim must be a multiple of 128");
   if (!(c->rope_theta > 0.f)) return fail(NOVA_EINVAL, "rope_theta must be positive");
   if (c->act != NOVA_ACT_BF16 && c->act != NOVA_ACT_F32) return fail(NOVA_EINVAL, "act must be NOVA_ACT_BF16 or NOVA_ACT_F32");
@@ -780,18 +781,21 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
     p.ss_in = ss(2 * c.layers), p.ss_parts = tiles, p.eps = c.eps;
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   } else {
-    // Larger batches: a residual + RMSNorm kernel sums the O / down split-K partials into x and
-    // writes the normalised rows for the next projection.
+    // Larger batches: a column-parallel fold kernel sums the O / down split-K partials into x,
+    // writes x * gain and per-64-column sums of squares, and the consumer projections normalise
+    // from those parts as above.
     const int sp_o = nova::gemv_splits(H, qd, B, f32, cus);
     const int sp_down = nova::gemv_splits(H, m->ip, B, f32, cus);
-    CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(nullptr, 0, ids, B, (const bf16_t*)m->d.embed, H, d.x, s));
-    CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(nullptr, 0, d.x, B, H, c.layers > 0 ? layer_w(0, 0) : final_gain, c.eps,
-                                                   d.a, H, c.layers > 0 ? nullptr : d.keys, s));
+    auto ss = [&](int k) { return d.ss + (size_t)k * tiles * B; };
+    CALL(NOVA_KIND_MISC, s, nova::decode_embed<T>(ids, B, (const bf16_t*)m->d.embed, H,
+                                                  c.layers > 0 ? layer_w(0, 0) : final_gain, d.x, d.a, ss(0), tiles, d.keys,
+                                                  nullptr, 0, s));
     for (int l = 0; l < c.layers; ++l) {
       auto W = [&](int i) { return layer_w(l, i); };
       {
         GemvArgs p{d.a, H, W(1), H, B, m->qkvw, H, sp_qkv > 1 ? nullptr : d.qkv, m->qkvw, d.part, nullptr};
         p.cus = cus;
+        p.ss_in = ss(2 * l), p.ss_parts = tiles, p.eps = c.eps;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_STORE, s)));
       }
       if (const int rc = attention_block(l)) return rc;
@@ -800,11 +804,12 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
         p.cus = cus;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
       }
-      CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_o > 1 ? d.part : nullptr, sp_o > 1 ? sp_o : 0, d.x, B, H, W(3), c.eps,
-                                                     d.a, H, nullptr, s));
+      CALL(NOVA_KIND_MISC, s, nova::resid_fold<T>(sp_o > 1 ? d.part : nullptr, sp_o > 1 ? sp_o : 0, d.x, B, H, W(3), d.a, H,
+                                                  ss(2 * l + 1), s));
       {
         GemvArgs p{d.a, H, W(4), H, B, 2 * m->ip, H, d.hm, m->ip, d.part, nullptr};
         p.cus = cus;
+        p.ss_in = ss(2 * l + 1), p.ss_parts = tiles, p.eps = c.eps;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, T>(p, nova::EPI_SWIGLU, s)));
       }
       {
@@ -812,12 +817,13 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
         p.cus = cus;
         CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_RESID, s)));
       }
-      CALL(NOVA_KIND_MISC, s, nova::resid_rmsnorm<T>(sp_down > 1 ? d.part : nullptr, sp_down > 1 ? sp_down : 0, d.x, B, H,
-                                                     l + 1 < c.layers ? layer_w(l + 1, 0) : final_gain, c.eps, d.a, H,
-                                                     l + 1 < c.layers ? nullptr : d.keys, s));
+      CALL(NOVA_KIND_MISC, s, nova::resid_fold<T>(sp_down > 1 ? d.part : nullptr, sp_down > 1 ? sp_down : 0, d.x, B, H,
+                                                  l + 1 < c.layers ? layer_w(l + 1, 0) : final_gain, d.a, H,
+                                                  ss(2 * l + 2), s));
     }
     GemvArgs p{d.a, H, (const bf16_t*)(hw + m->head.off[1]), H, B, c.vocab, H, logits_out, c.vocab, d.part, d.keys};
     p.cus = cus;
+    p.ss_in = ss(2 * c.layers), p.ss_parts = tiles, p.eps = c.eps;
     CALL(NOVA_KIND_GEMV, s, (nova::gemv<T, float>(p, nova::EPI_ARGMAX, s)));
   }
   CALL(NOVA_KIND_MISC, s, nova::argmax_finish(d.keys, B, next_ids, s));
