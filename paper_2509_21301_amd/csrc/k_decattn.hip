@@ -33,15 +33,23 @@ size_t dec_attn_partial_floats(int B, int n_q, int D, int max_ctx, int n_kv) {
   return (size_t)B * n_q * s * (D + 2);
 }
 
+// Raw registers of one block pair: K rows (token col, 8 dims per 32-dim step) and V^T rows
+// (dim 16i + col, tokens 4grp..+3) of both blocks, with the blocks' physical ids (-1: none).
+template <bool F32, int NS, int ND> struct DaPair;
+template <int NS, int ND> struct DaPair<false, NS, ND> { Frag8 k[2][NS]; uint2 v[ND][2]; int ph[2]; };
+template <int NS, int ND> struct DaPair<true, NS, ND> { float4 k[2][NS][2]; float4 v[ND][2]; int ph[2]; };
+
 template <typename T, int D>
-__global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_per_split) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) dec_attn_kernel(DecAttnArgs p, int pairs_per_split) {
   constexpr bool F32 = sizeof(T) == 4;
   constexpr int NS = D / 32;      // k-steps of S = K Q^T
   constexpr int ND = D / 16;      // output row blocks of O^T
+  using Pair = DaPair<F32, NS, ND>;
   __shared__ float sm_m[4][16], sm_l[4][16];
   __shared__ float sm_o[4][D][16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int G = p.n_q / p.n_kv;
   const int col = lane & 15, grp = lane >> 4;
@@ -52,6 +60,47 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
   const T* kpool = reinterpret_cast<const T*>(p.kpool);
   const T* vpool = reinterpret_cast<const T*>(p.vpool);
   const int* table = p.tables + (size_t)b * p.max_blocks;
+  // this wave takes pairs first, first + 4, ...: iteration it covers pair first + 4 it
+  const int first = pair_begin + wave;
+  const int n_it = first < pair_end ? (pair_end - first + 3) / 4 : 0;
+
+  // block-table entries of 32 iterations at a time, one per lane (lane 2i + j: block j of
+  // iteration i), read back with a uniform lane index, so the K/V loads of a pair wait for no
+  // table load of their own
+  int tl = -1, tl_chunk = -1;
+  auto phys_of = [&](int it, int j) -> int {
+    if ((it >> 5) != tl_chunk) {
+      tl_chunk = it >> 5;
+      const int pr = first + 4 * (32 * tl_chunk + (lane >> 1));
+      const int blk = 2 * pr + (lane & 1);
+      tl = (pr < pair_end && blk < nblk) ? table[blk] : -1;
+    }
+    return __builtin_amdgcn_readlane(tl, 2 * (it & 31) + j);
+  };
+  // every load of a pair is issued together (addresses clamped to block 0 where a block is absent)
+  auto load = [&](int it, Pair& r) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      r.ph[j] = phys_of(it, j);
+      const size_t base = ((size_t)max(r.ph[j], 0) * p.n_kv + kvh) * DA_BLOCK * D;
+      const T* kb = kpool + base + (size_t)col * D + 8 * grp;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        if constexpr (F32) {
+          r.k[j][s][0] = *reinterpret_cast<const float4*>(kb + 32 * s);
+          r.k[j][s][1] = *reinterpret_cast<const float4*>(kb + 32 * s + 4);
+        } else {
+          r.k[j][s] = *reinterpret_cast<const Frag8*>(kb + 32 * s);
+        }
+      }
+      const T* vb = vpool + base + (size_t)col * DA_BLOCK + 4 * grp;
+#pragma unroll
+      for (int i = 0; i < ND; ++i) {
+        if constexpr (F32) r.v[i][j] = *reinterpret_cast<const float4*>(vb + (size_t)16 * i * DA_BLOCK);
+        else r.v[i][j] = *reinterpret_cast<const uint2*>(vb + (size_t)16 * i * DA_BLOCK);
+      }
+    }
+  };
 
   // Q^T fragments: head col of this group, dims 32s + 8grp .. +8 (zero for col >= G)
   Frag8 qh[NS], ql[F32 ? NS : 1];
@@ -79,60 +128,43 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
   float m_run = -1e30f, l_run = 0.f;
   const float scale = 1.4426950408889634f / sqrtf((float)D);
 
-  for (int pr = pair_begin + wave; pr < pair_end; pr += 4) {
+  auto compute = [&](int it, const Pair& r) {
+    const int pr = first + 4 * it;
     f32x4 sc[2];
-    int phys[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int blk = 2 * pr + j;
-      phys[j] = blk < nblk ? table[blk] : -1;
       sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (phys[j] < 0) continue;
-      const T* kb = kpool + ((size_t)phys[j] * p.n_kv + kvh) * DA_BLOCK * D;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const T* src = kb + (size_t)col * D + 32 * s + 8 * grp;     // token col, dims 32s+8grp..
         if constexpr (F32) {
           float x[8];
-          *reinterpret_cast<float4*>(x) = *reinterpret_cast<const float4*>(src);
-          *reinterpret_cast<float4*>(x + 4) = *reinterpret_cast<const float4*>(src + 4);
+          *reinterpret_cast<float4*>(x) = r.k[j][s][0];
+          *reinterpret_cast<float4*>(x + 4) = r.k[j][s][1];
           Frag8 kh, kl;
           split8(x, kh, kl);
           sc[j] = mfma16(kh, qh[s], sc[j]);
           sc[j] = mfma16(kl, qh[s], sc[j]);
           sc[j] = mfma16(kh, ql[s], sc[j]);
         } else {
-          Frag8 ka = *reinterpret_cast<const Frag8*>(src);
-          sc[j] = mfma16(ka, qh[s], sc[j]);
+          sc[j] = mfma16(r.k[j][s], qh[s], sc[j]);
         }
       }
     }
-    // V^T fragments of both blocks, loaded now so that their latency overlaps the softmax: row
-    // d = 16i + col, tokens 4grp..+3 of each block (zero past the table)
-    uint2 vraw[ND][2];
-    float4 vraw32[F32 ? ND : 1][2];
-#pragma unroll
-    for (int i = 0; i < ND; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const T* src = vpool + ((size_t)max(phys[j], 0) * p.n_kv + kvh) * D * DA_BLOCK + (size_t)(16 * i + col) * DA_BLOCK + 4 * grp;
-        if constexpr (F32) {
-          vraw32[i][j] = phys[j] >= 0 ? *reinterpret_cast<const float4*>(src) : float4{0.f, 0.f, 0.f, 0.f};
-        } else {
-          vraw[i][j] = phys[j] >= 0 ? *reinterpret_cast<const uint2*>(src) : make_uint2(0u, 0u);
-        }
-      }
-    // lane holds S[token 4*grp + r][head col] for block j; mask tokens beyond the context
+    // lane holds S[token 4*grp + q][head col] for block j; mask tokens beyond the context (and
+    // absent blocks: the K rows read there are block 0's, replaced by -inf here)
     float tmax = -1e30f;
+    int nvalid[2];       // tokens 4grp..+3 of block j inside the context
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 2; ++j) {
+      const int t0 = (2 * pr + j) * DA_BLOCK + 4 * grp;
+      nvalid[j] = r.ph[j] < 0 ? 0 : min(max(ctx - t0, 0), 4);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tok = (2 * pr + j) * DA_BLOCK + 4 * grp + r;
-        const float v = (phys[j] >= 0 && tok < ctx) ? sc[j][r] * scale : -INFINITY;
-        sc[j][r] = v;
+      for (int q = 0; q < 4; ++q) {
+        const float v = q < nvalid[j] ? sc[j][q] * scale : -INFINITY;
+        sc[j][q] = v;
         tmax = fmaxf(tmax, v);
       }
+    }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float m_new = fmaxf(m_run, tmax);
@@ -142,9 +174,9 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        pv[4 * j + r] = exp2f(sc[j][r] - m_new);
-        rs += pv[4 * j + r];
+      for (int q = 0; q < 4; ++q) {
+        pv[4 * j + q] = exp2f(sc[j][q] - m_new);
+        rs += pv[4 * j + q];
       }
     rs += __shfl_xor(rs, 16, 64);
     rs += __shfl_xor(rs, 32, 64);
@@ -157,29 +189,54 @@ __global__ void __launch_bounds__(256) dec_attn_kernel(DecAttnArgs p, int pairs_
 #pragma unroll
       for (int e = 0; e < 4; ++e) ph.w[e] = pack2(pv[2 * e], pv[2 * e + 1]);
     }
+    // V^T values of tokens outside the context are zeroed (their probabilities are zero, but the
+    // cache slots past the last written token may hold anything, NaN included)
+    uint32_t vmask[2][2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const unsigned long long m = nvalid[j] >= 4 ? ~0ull : ((1ull << (16 * nvalid[j])) - 1ull);
+      vmask[j][0] = (uint32_t)m;
+      vmask[j][1] = (uint32_t)(m >> 32);
+    }
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
       o[i][0] *= corr; o[i][1] *= corr; o[i][2] *= corr; o[i][3] *= corr;
       // V^T fragment: row d = 16i + col, same tokens as the P^T fragment
-      float vx[8];
-      Frag8 va, vl;
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        if constexpr (F32) {
-          *reinterpret_cast<float4*>(vx + 4 * j) = vraw32[i][j];
-        } else {
-          va.w[2 * j] = vraw[i][j].x; va.w[2 * j + 1] = vraw[i][j].y;
-        }
-      }
       if constexpr (F32) {
+        float vx[8];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          vx[4 * j + 0] = nvalid[j] > 0 ? r.v[i][j].x : 0.f;
+          vx[4 * j + 1] = nvalid[j] > 1 ? r.v[i][j].y : 0.f;
+          vx[4 * j + 2] = nvalid[j] > 2 ? r.v[i][j].z : 0.f;
+          vx[4 * j + 3] = nvalid[j] > 3 ? r.v[i][j].w : 0.f;
+        }
+        Frag8 va, vl;
         split8(vx, va, vl);
         o[i] = mfma16(va, ph, o[i]);
         o[i] = mfma16(vl, ph, o[i]);
         o[i] = mfma16(va, pl, o[i]);
       } else {
+        Frag8 va;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          va.w[2 * j] = r.v[i][j].x & vmask[j][0];
+          va.w[2 * j + 1] = r.v[i][j].y & vmask[j][1];
+        }
         o[i] = mfma16(va, ph, o[i]);
       }
     }
+  };
+
+  // two register sets: the loads of the next pair are in flight while this pair is computed
+  Pair ra, rb;
+  if (n_it > 0) load(0, ra);
+  for (int it = 0; it < n_it; it += 2) {
+    if (it + 1 < n_it) load(it + 1, rb);
+    compute(it, ra);
+    if (it + 1 >= n_it) break;
+    if (it + 2 < n_it) load(it + 2, ra);
+    compute(it + 1, rb);
   }
 
   // merge the four waves: lane holds O^T[d = 16i + 4grp + r][head col]
@@ -256,7 +313,9 @@ hipError_t decode_attention(const DecAttnArgs& p, int head_dim, hipStream_t s) {
     return hipErrorInvalidValue;
   switch (head_dim) {
     case 64: return dec_launch<T, 64>(p, s);
-    case 128: return dec_launch<T, 128>(p, s);
+    case 128:
+      if constexpr (sizeof(T) == 4) return hipErrorInvalidValue;   // the fp32 mode stops at head_dim 80
+      else return dec_launch<T, 128>(p, s);
   }
   return hipErrorInvalidValue;
 }
