@@ -107,9 +107,12 @@ def test_prefill_layer_real_width(gpu_lib, llm1, nv, nt):
 
 
 # the thin GEMMs split K by the stream's CU count: on a 64-CU partition the O and down
-# projections run unsplit, the residual update and the folded norm in the direct epilogue
-@pytest.mark.parametrize("bsz,cus", [(4, None), (20, None), (4, 64), (20, 64)])
-def test_decode_real_width(gpu_lib, llm1, bsz, cus):
+# projections run unsplit, the residual update and the folded norm in the direct epilogue.
+# nan_tail: the cache slots after each sequence's new token (never written, never attended)
+# hold NaN, which must not reach the outputs
+@pytest.mark.parametrize("bsz,cus,nan_tail", [(4, None, False), (20, None, False), (4, 64, False), (20, 64, False),
+                                              (20, None, True)])
+def test_decode_real_width(gpu_lib, llm1, bsz, cus, nan_tail):
     import torch
     nova = gpu_lib
     w, llm = llm1
@@ -120,6 +123,10 @@ def test_decode_real_width(gpu_lib, llm1, bsz, cus):
     kref = vlm.PagedKV(cfg.layers, pool, cfg.n_kv, cfg.block, cfg.head_dim)
     kref.k[:] = synth.bf16_round(rng.standard_normal(kref.k.shape, dtype=np.float32))
     kref.v[:] = synth.bf16_round(rng.standard_normal(kref.v.shape, dtype=np.float32))
+    if nan_tail:
+        for b, c in enumerate(ctx):
+            kref.k[:, tables[b][c // cfg.block], :, c % cfg.block + 1:, :] = np.nan
+            kref.v[:, tables[b][c // cfg.block], :, c % cfg.block + 1:, :] = np.nan
     kv = nova.KvPool(llm, pool)
     kv.k5.copy_(torch.from_numpy(kref.k.astype(np.float32)).to(torch.bfloat16))
     kv.v5.copy_(torch.from_numpy(np.swapaxes(kref.v, -1, -2).astype(np.float32)).to(torch.bfloat16))
@@ -139,5 +146,11 @@ def test_decode_real_width(gpu_lib, llm1, bsz, cus):
         top = np.sort(ref_logits[b])[::-1]
         if top[0] - top[1] > 2 * np.abs(got[b] - ref_logits[b]).max():
             assert got_ids[b] == ref_ids[b], f"seq {b}"
-    ek, ev = sc.kv_errors(kref.k, kref.v, kv.k5.float().cpu().numpy(), kv.v5.float().cpu().numpy())
+    assert np.isfinite(got).all()
+    gk, gv = kv.k5.float().cpu().numpy(), kv.v5.float().cpu().numpy()
+    if nan_tail:   # the NaN slots must still be NaN on both sides (nothing wrote there), then compare the rest
+        assert np.array_equal(np.isnan(gk), np.isnan(kref.k))
+        assert np.array_equal(np.isnan(np.swapaxes(gv, -1, -2)), np.isnan(kref.v))
+        kref.k, kref.v, gk, gv = (np.nan_to_num(a) for a in (kref.k, kref.v, gk, gv))
+    ek, ev = sc.kv_errors(kref.k, kref.v, gk, gv)
     assert ek < sc.TOL_BF16 and ev < sc.TOL_BF16
