@@ -389,7 +389,8 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   const int sw = (fr >> 1) & 7;
   const int off0 = fr * BK + 8 * (fk ^ sw);          // elements, sub-step 0
   const int off1 = fr * BK + 8 * ((fk + 4) ^ sw);    // sub-step 1
-  const int nk = (p.kslice ? p.kslice : p.K) / BK;
+  // K slices are kslice long except the last, which takes what remains
+  const int nk = (p.kslice ? min(p.kslice, p.K - (int)k_off) : p.K) / BK;
   dma(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -543,6 +544,33 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
     // without the split partials' traffic
     if (p.N % 256 == 0 && p.K >= 8192 && tiles256 >= 192 && tiles256 <= 256)
       return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
+    // a very long K whose 256x256 tiles fill under three quarters of the GPU (the 1500-token
+    // prefill's down projection: 6 x 14 tiles, K = 18944): K slices of 256x256 tiles that make one
+    // round of at least 224 of the 256 CUs (3 slices of 6336, 6336 and 6272 there), then the
+    // fp32 partials summed in slice order
+    if (p.split_ws && p.N % 256 == 0 && p.K >= 8192 && tiles256 < 192) {
+      int sl = 0;
+      for (int c = 2; c <= 4 && !sl; ++c) {
+        const int kslice = (p.K / BK + c - 1) / c * BK;
+        if (tiles256 * c >= 224 && tiles256 * c <= 256 && p.K - (c - 1) * kslice >= 1024 &&
+            (size_t)c * p.M * p.N <= p.split_ws_floats)
+          sl = c;
+      }
+      if (sl) {
+        GemmArgs q = p;
+        q.out = p.split_ws;
+        q.ldo = p.N;
+        q.kslice = (p.K / BK + sl - 1) / sl * BK;
+        q.split_stride = (long)p.M * p.N;
+        q.vt = nullptr;
+        hipError_t e = launch_dma<float, EPI_STORE, 256, 256, 64, 128>(q, s, sl);
+        if (e != hipSuccess) return e;
+        const long n4 = (long)p.M * (p.N / 4);
+        hipLaunchKernelGGL((split_reduce_kernel<OT, EPI>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, p,
+                           (const float*)p.split_ws, sl);
+        return hipGetLastError();
+      }
+    }
     if (!(p.N % 256 == 0 && tiles256 >= 512)) {
       const int sl = split_slices(p);
       if (sl > 1) {
