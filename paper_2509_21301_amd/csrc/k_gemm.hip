@@ -536,7 +536,8 @@ template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when there are at least two tiles per
   // CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU), with K split into slices
-  // when those tiles cannot fill the GPU (and the caller gave a workspace).
+  // when those tiles cannot fill the GPU (and the caller gave a workspace).  A projection that
+  // also stores V^T (p.vt) always runs as one launch: the split paths have no V^T epilogue.
   if constexpr (sizeof(TA) == 2 && (EPI == EPI_STORE || EPI == EPI_RESID)) {
     const long tiles256 = (long)((p.M + 255) / 256) * (p.N / 256);
     // a very long K whose 256x256 tiles make one round of at least three quarters of the GPU
@@ -548,7 +549,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
     // prefill's down projection: 6 x 14 tiles, K = 18944): K slices of 256x256 tiles that make one
     // round of at least 224 of the 256 CUs (3 slices of 6336, 6336 and 6272 there), then the
     // fp32 partials summed in slice order
-    if (p.split_ws && p.N % 256 == 0 && p.K >= 8192 && tiles256 < 192) {
+    if (p.split_ws && p.vt == nullptr && p.N % 256 == 0 && p.K >= 8192 && tiles256 < 192) {
       int sl = 0;
       for (int c = 2; c <= 4 && !sl; ++c) {
         const int kslice = (p.K / BK + c - 1) / c * BK;
@@ -571,7 +572,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         return hipGetLastError();
       }
     }
-    if (!(p.N % 256 == 0 && tiles256 >= 512)) {
+    if (!(p.N % 256 == 0 && tiles256 >= 512) && p.vt == nullptr) {
       const int sl = split_slices(p);
       if (sl > 1) {
         GemmArgs q = p;
@@ -598,7 +599,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
       // last round is not left mostly idle
       const long rounds = tiles / 256;
       const int n1 = (int)(rounds * 256 / nm) * 256;
-      if (tiles % 256 >= 32 && nm <= 16 && n1 < p.N && EPI != EPI_POS) {
+      if (tiles % 256 >= 32 && nm <= 16 && n1 < p.N && EPI != EPI_POS && p.vt == nullptr) {
         GemmArgs a = p;
         a.N = n1;
         hipError_t e = launch_dma<OT, EPI, 256, 256, 64, 128>(a, s);

@@ -340,22 +340,40 @@ class Llm:
         _check(lib.nova_llm_create(C.byref(desc), C.byref(h)))
         self.h = h
         self._ws = {}
+        self._retired = []
 
-    def _workspace(self, key, nbytes):
+    def _workspace(self, key, nbytes, stream=None):
         t = self._ws.get(key)
         if t is None or t.numel() < nbytes:
             if t is not None:
-                # the old buffer may still be in use by work queued on another stream than the one
-                # torch's allocator files it under: let that work finish before it is released
-                torch.cuda.synchronize(self.device)
+                # the old buffer may still be read by work queued earlier by this stage; keep it
+                # until an event recorded now on this call's stream has completed (the library
+                # orders a stage's new partition stream after its earlier ones), so the caching
+                # allocator cannot hand it out while the GPU still uses it
+                ev = torch.cuda.Event()
+                ev.record(stream if stream is not None else torch.cuda.current_stream())
+                self._retired.append((t, ev))
             t = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
             self._ws[key] = t
+        if self._retired:
+            self._retired = [(b, e) for b, e in self._retired if not e.query()]
         return t
+
+    def reserve(self, prefill_tokens=0, decode_batch=0, decode_ctx=0):
+        """Size the prefill and decode workspaces once for the largest calls to come, so that no
+        later call grows them (a serving worker then never waits on a buffer swap)."""
+        if prefill_tokens > 0:
+            self._workspace("prefill", lib.nova_llm_prefill_workspace_bytes(self.h, prefill_tokens))
+        if decode_batch > 0 and decode_ctx > 0:
+            # the attention split count falls with the batch, so the largest need is not always at
+            # the largest batch
+            need = max(lib.nova_llm_decode_workspace_bytes(self.h, b, decode_ctx) for b in range(1, decode_batch + 1))
+            self._workspace("decode", need)
 
     def prefill(self, vis, ids, table, kv, logits=None, next_id=None, stream=None):
         n_vis = 0 if vis is None else vis.shape[0]
         n_text = ids.shape[0]
-        ws = self._workspace("prefill", lib.nova_llm_prefill_workspace_bytes(self.h, n_vis + n_text))
+        ws = self._workspace("prefill", lib.nova_llm_prefill_workspace_bytes(self.h, n_vis + n_text), stream)
         if next_id is None:
             next_id = torch.empty(1, dtype=torch.int32, device=self.device)
         _check(lib.nova_llm_prefill(self.h, _ptr(vis), n_vis, _ptr(ids), n_text, _ptr(table), C.byref(kv.c),
@@ -364,7 +382,8 @@ class Llm:
 
     def decode(self, ids, pos, tables, kv, max_ctx, next_ids=None, logits=None, stream=None):
         b = ids.shape[0]
-        ws = self._workspace(("decode", b), lib.nova_llm_decode_workspace_bytes(self.h, b, max_ctx))
+        # one decode workspace for every batch size: a larger one serves a smaller step as well
+        ws = self._workspace("decode", lib.nova_llm_decode_workspace_bytes(self.h, b, max_ctx), stream)
         if next_ids is None:
             next_ids = torch.empty(b, dtype=torch.int32, device=self.device)
         _check(lib.nova_llm_decode(self.h, _ptr(ids), _ptr(pos), _ptr(tables), tables.shape[1], b, max_ctx,

@@ -9,8 +9,10 @@ batching); partitions change only at forward-pass boundaries.  Partition modes:
 * ``nova``         -- decode holds P CUs while co-running, the other stage 256 - P (static P,
                       or Eq. 5 from the number of requests in vision/prefill);
 * ``multi_stream`` -- the same worker threads on unrestricted streams (the paper's Multi-Stream);
-* ``time_sliced``  -- one worker runs one forward pass at a time on the whole GPU, alternating a
-                      decode step with each encode/prefill pass.
+* ``time_sliced``  -- one worker runs one forward pass at a time on the whole GPU, in one of three
+                      orders: a decode step between encode/prefill passes, decode first, or
+                      encode/prefill first (optionally with the PF-Limit decode threshold of the
+                      paper's Sec. 5.1 baselines).
 
 Every worker is a thread that enqueues its pass on its stream through the C ABI and waits for
 it; the scheduler thread owns the request state.  All timing is wall clock.
@@ -83,11 +85,16 @@ class BlockPool:
 
 class Server:
     def __init__(self, vit, llm, kv, pixels, mode="nova", decode_cus=(96, 96), alpha=0, minimum=32, max_batch=32,
-                 max_blocks=256, device="cuda"):
+                 max_blocks=256, device="cuda", slice_order="alternate", decode_limit=None):
         """decode_cus = (P_v, P_p): decode's CUs while co-running with vision encode / prefill
-        (Eq. 3's optimum); alpha > 0 turns on the Eq. 5 adaptation with floor `minimum`."""
+        (Eq. 3's optimum); alpha > 0 turns on the Eq. 5 adaptation with floor `minimum`.
+        slice_order / decode_limit choose the time-sliced driver's pass order (see
+        _slice_decode_next)."""
+        if slice_order not in ("alternate", "decode_first", "prefill_first"):
+            raise ValueError(f"unknown slice_order {slice_order!r}")
         self.vit, self.llm, self.kv, self.pixels, self.device = vit, llm, kv, pixels, device
         self.mode, self.decode_cus, self.alpha, self.minimum = mode, decode_cus, alpha, minimum
+        self.slice_order, self.decode_limit = slice_order, decode_limit
         self.other = None             # stage co-running with decode: STAGE_ENCODE, STAGE_PREFILL or None
         self.max_batch, self.max_blocks = max_batch, max_blocks
         self.cfg = llm.cfg
@@ -98,6 +105,10 @@ class Server:
         self.lock = threading.Lock()
         self.n_pending = 0            # requests queued for or inside vision encode / prefill
         self.decode_active = 0        # requests in the decode batch or waiting to join it
+        reserve = getattr(llm, "reserve", None)
+        if reserve is not None:       # workspaces sized once, before any timed pass
+            reserve(prefill_tokens=max_blocks * self.cfg.block, decode_batch=max_batch,
+                    decode_ctx=max_blocks * self.cfg.block)
         self.partition_log = []
         self.decode_batches = []      # batch size of every decode step
         self.sched_us = []            # scheduler time per handled event (host, microseconds)
@@ -146,13 +157,21 @@ class Server:
             req.last_token = int(nxt.item())
         req.t_pre1 = time.perf_counter()
 
+    def _decode_positions(self, batch):
+        """Position of the token each request feeds in its next decode step, and the step's max_ctx.
+
+        Prefill writes positions 0..S-1 (S = visual + text tokens) and emits token 0; decode step
+        t feeds token t at position S + t, so a request that holds k generated tokens feeds its
+        last one at S + k - 1 and attends to S + k keys."""
+        pos = [self.n_vis + r.n_text + len(r.t_tokens) - 1 for r in batch]
+        return pos, max(pos) + 1
+
     def _decode_step(self, batch):
         s = self._stream(nova.STAGE_DECODE)
-        b = len(batch)
         ids = torch.tensor([r.last_token for r in batch], dtype=torch.int32)
-        pos = torch.tensor([self.n_vis + r.n_text + len(r.t_tokens) for r in batch], dtype=torch.int32)
+        pos_l, max_ctx = self._decode_positions(batch)
+        pos = torch.tensor(pos_l, dtype=torch.int32)
         tab = torch.from_numpy(np.stack([r.table_row for r in batch]))
-        max_ctx = int(pos.max()) + 1
         with torch.cuda.stream(s):
             ids_d, pos_d, tab_d = ids.cuda(non_blocking=True), pos.cuda(non_blocking=True), tab.cuda(non_blocking=True)
             nxt = self.llm.decode(ids_d, pos_d, tab_d, self.kv, max_ctx, stream=s)
@@ -187,6 +206,18 @@ class Server:
     def _run_threads(self, trace):
         vq, pq, dq = queue.Queue(), queue.Queue(), queue.Queue()
         stop = threading.Event()
+        abort = threading.Event()
+
+        def guarded(body):
+            # a failed launch or a HIP error inside a worker must end the run, not leave the
+            # scheduler waiting for an event that never comes
+            def run():
+                try:
+                    body()
+                except BaseException as exc:          # noqa: BLE001 -- re-raised by the scheduler
+                    abort.set()
+                    self.events.put(("error", exc))
+            return run
 
         def vision_worker():
             while True:
@@ -207,6 +238,8 @@ class Server:
         def decode_worker():
             batch, waiting = [], []
             while not stop.is_set() or batch or waiting or not dq.empty():
+                if abort.is_set():
+                    return
                 try:
                     while True:
                         waiting.append(dq.get(block=not batch and not waiting, timeout=0.01))
@@ -222,7 +255,7 @@ class Server:
                     batch.remove(r)
                     self.events.put(("finished", r))
 
-        threads = [threading.Thread(target=f, daemon=True) for f in (vision_worker, prefill_worker, decode_worker)]
+        threads = [threading.Thread(target=guarded(f), daemon=True) for f in (vision_worker, prefill_worker, decode_worker)]
         for t in threads:
             t.start()
         t0 = time.perf_counter()
@@ -254,6 +287,13 @@ class Server:
             except queue.Empty:
                 continue
             t_ev = time.perf_counter()
+            if ev == "error":
+                stop.set()
+                vq.put(None)
+                pq.put(None)
+                for t in threads:
+                    t.join(timeout=30)
+                raise RuntimeError(f"serving worker failed: {r!r}") from r
             if ev == "vision_done":
                 busy["vision"] = False
                 busy["prefill"] = True            # prefill goes first, before any further vision
@@ -285,6 +325,23 @@ class Server:
             t.join(timeout=30)
         return self._summary(trace)
 
+    def _slice_decode_next(self, n_batch, n_decode, other_ready, last_was_decode):
+        """Whether the time-sliced driver runs a decode step next (rather than an encode/prefill pass).
+
+        ``alternate``: a decode step between any two encode/prefill passes; ``decode_first``: decode
+        whenever a batch is active; ``prefill_first``: encode/prefill whenever one is queued, decode
+        otherwise, or (with ``decode_limit``, the paper's PF-Limit baseline) also once more than
+        ``decode_limit`` requests are in the decode stage."""
+        if n_batch == 0:
+            return False
+        if not other_ready:
+            return True
+        if self.slice_order == "decode_first":
+            return True
+        if self.slice_order == "prefill_first":
+            return self.decode_limit is not None and n_decode > self.decode_limit
+        return not last_was_decode
+
     def _run_sliced(self, trace):
         t0 = time.perf_counter()
         pending = list(trace)
@@ -298,7 +355,8 @@ class Server:
                 q_vision.append(r)
             while q_decode and len(batch) < self.max_batch:   # join at a step boundary
                 batch.append(q_decode.pop(0))
-            if batch and (not last_was_decode or (not q_prefill and not q_vision)):
+            if self._slice_decode_next(len(batch), len(batch) + len(q_decode), bool(q_prefill or q_vision),
+                                       last_was_decode):
                 self.decode_batches.append(len(batch))
                 self._decode_step(batch)
                 last_was_decode = True

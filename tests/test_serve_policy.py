@@ -11,12 +11,12 @@ import pytest
 from paper_2509_21301_amd import serve, synth
 
 
-def fake_server(mode):
+def fake_server(mode, **kw):
     cfg = synth.TINY_LLM
     vit = SimpleNamespace(cfg=SimpleNamespace(n_out=64))
     llm = SimpleNamespace(cfg=cfg)
     kv = SimpleNamespace(num_blocks=2000)
-    srv = serve.Server(vit, llm, kv, None, mode=mode, max_batch=4, max_blocks=64, device="cpu")
+    srv = serve.Server(vit, llm, kv, None, mode=mode, max_batch=4, max_blocks=64, device="cpu", **kw)
     log, lock = [], threading.Lock()
     active = {"vision": 0, "prefill": 0, "decode": 0, "any": 0}
 
@@ -46,19 +46,27 @@ def fake_server(mode):
 
     def decode(batch):
         assert len(batch) <= 4
+        pos, max_ctx = srv._decode_positions(batch)      # what the real step hands the library
         span("decode", 0.003)
         now = time.perf_counter()
-        for r in batch:
+        for r, p in zip(batch, pos):
             r.t_tokens.append(now)
+            srv.fed_positions.setdefault(r.rid, []).append((p, max_ctx))
         log.append(("decode", tuple(r.rid for r in batch)))
 
     srv._vision, srv._prefill, srv._decode_step = vision, prefill, decode
+    srv.fed_positions = {}
     return srv, log
 
 
-@pytest.mark.parametrize("mode", ["nova", "time_sliced"])
+SLICED = {"sliced_alternate": dict(slice_order="alternate"), "sliced_decode_first": dict(slice_order="decode_first"),
+          "sliced_prefill_first": dict(slice_order="prefill_first"),
+          "pf_limit": dict(slice_order="prefill_first", decode_limit=5)}
+
+
+@pytest.mark.parametrize("mode", ["nova", *SLICED])
 def test_alg1_policy(mode):
-    srv, log = fake_server(mode)
+    srv, log = fake_server("nova" if mode == "nova" else "time_sliced", **SLICED.get(mode, {}))
     trace = serve.poisson_trace(rate=200.0, window_s=0.08, seed=1, n_text=(5, 9), n_out=(6, 12))
     assert len(trace) >= 8
     res = srv.run(trace)
@@ -68,7 +76,7 @@ def test_alg1_policy(mode):
         assert r.t_arrive <= r.t_vis0 <= r.t_vis1 <= r.t_pre1 <= r.t_tokens[0]
     starts = [e[2] for e in log if e[0] == "start"]
     assert all(a["vision"] + a["prefill"] <= 1 for a in starts)          # never vision with prefill
-    if mode == "time_sliced":
+    if mode != "nova":
         assert all(a["any"] <= 1 for a in starts)                        # one pass at a time
     order = [e for e in log if e[0] in ("vision", "prefill")]
     vis = [e[1] for e in order if e[0] == "vision"]
@@ -77,7 +85,16 @@ def test_alg1_policy(mode):
         if e[0] == "vision":
             assert order[i + 1] == ("prefill", e[1])
     batches = [e[1] for e in log if e[0] == "decode"]
-    assert max(len(b) for b in batches) > 1                              # in-flight batching happened
+    if mode != "sliced_decode_first":     # decode-first finishes each batch before the next prefill
+        assert max(len(b) for b in batches) > 1                          # in-flight batching happened
+    # decode step t of a request feeds token t at position S + t (prefill wrote 0..S-1 and emitted
+    # token 0), and the step's max_ctx covers every sequence of the batch
+    for r in trace:
+        s_len = 64 + r.n_text
+        fed = srv.fed_positions[r.rid]
+        assert [p for p, _ in fed] == list(range(s_len, s_len + r.n_out - 1)), r.rid
+        assert all(p < m for p, m in fed)
+        assert (s_len + r.n_out - 2) // 16 < len(r.blocks)                 # the last fed position has a block
     assert srv.blocks.free and len(srv.blocks.free) == 2000             # every KV block returned
     assert res["max_e2e_s"] >= res["avg_e2e_s"] > 0
     # statistics: decode batch sizes of every step, Eq. 6 beside the measured vision-queue wait
@@ -86,6 +103,39 @@ def test_alg1_policy(mode):
     assert res["mean_service_s"] > 0 and "eq6_predicted_wait_s" in res
     if mode == "nova":
         assert res["sched_event_us"]["events"] >= 2 * len(trace)
+
+
+def test_decode_positions_after_prefill():
+    srv, _ = fake_server("nova")
+    a = serve.Request(0, 0.0, n_text=10, n_out=5)
+    b = serve.Request(1, 0.0, n_text=30, n_out=5)
+    a.t_tokens = [0.1]                  # just prefilled: feeds token 0 at S = 64 + 10
+    b.t_tokens = [0.1, 0.2, 0.3]        # two decode steps done: feeds token 2 at S + 2
+    pos, max_ctx = srv._decode_positions([a, b])
+    assert pos == [74, 96] and max_ctx == 97
+
+
+@pytest.mark.parametrize("order,limit,n_batch,n_decode,other,last,want", [
+    ("alternate", None, 2, 2, True, False, True), ("alternate", None, 2, 2, True, True, False),
+    ("alternate", None, 0, 0, True, False, False), ("decode_first", None, 1, 1, True, True, True),
+    ("prefill_first", None, 3, 9, True, False, False), ("prefill_first", None, 3, 3, False, True, True),
+    ("prefill_first", 5, 4, 5, True, False, False), ("prefill_first", 5, 4, 6, True, True, True)])
+def test_time_sliced_orders(order, limit, n_batch, n_decode, other, last, want):
+    srv, _ = fake_server("time_sliced", slice_order=order, decode_limit=limit)
+    assert srv._slice_decode_next(n_batch, n_decode, other, last) is want
+
+
+def test_worker_error_ends_the_run():
+    srv, _ = fake_server("nova")
+
+    def broken(req):
+        raise RuntimeError("launch failed")
+    srv._vision = broken
+    trace = serve.poisson_trace(rate=200.0, window_s=0.05, seed=2, n_text=(5, 9), n_out=(6, 12))
+    t0 = time.perf_counter()
+    with pytest.raises(RuntimeError, match="serving worker failed"):
+        srv.run(trace)
+    assert time.perf_counter() - t0 < 10
 
 
 def test_block_pool_exhaustion_is_an_error():
