@@ -229,25 +229,42 @@ class PagedKV:
 # --------------------------------------------------------------------------------------
 # LLM prefill and decode
 # --------------------------------------------------------------------------------------
-def _qkv(h, w, l, cfg, pos):
+def bf16_store(x):
+    """A tensor as a bf16 model stores it: each value rounded to the nearest bfloat16 (ties to
+    even), returned as float64.  The paper runs its models in bf16 (Sec. 5.1), so the activations
+    a bf16 model keeps between operations and its KV cache hold bf16 values.  Values are taken to
+    float32 first (the precision the arithmetic between two stores works in), then rounded.
+    """
+    f = np.ascontiguousarray(np.asarray(x, F64), dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    r = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    out = r.astype(np.uint32).view(np.float32).astype(F64)
+    return np.where(np.isnan(f), np.nan, out)
+
+
+def _keep(x):
+    return x
+
+
+def _qkv(h, w, l, cfg, pos, store=_keep):
     p = f"l{l}."
     n = h.shape[0]
     d = cfg.head_dim
-    q = rope(linear(h, w[p + "q.w"]).reshape(n, cfg.n_q, d), pos, cfg.rope_theta)
-    k = rope(linear(h, w[p + "k.w"]).reshape(n, cfg.n_kv, d), pos, cfg.rope_theta)
-    v = linear(h, w[p + "v.w"]).reshape(n, cfg.n_kv, d)
+    q = store(rope(store(linear(h, w[p + "q.w"])).reshape(n, cfg.n_q, d), pos, cfg.rope_theta))
+    k = store(rope(store(linear(h, w[p + "k.w"])).reshape(n, cfg.n_kv, d), pos, cfg.rope_theta))
+    v = store(linear(h, w[p + "v.w"])).reshape(n, cfg.n_kv, d)
     return q, k, v
 
 
-def _mlp(x, w, l, cfg):
+def _mlp(x, w, l, cfg, store=_keep):
     p = f"l{l}."
-    h = rms_norm(x, w[p + "rms2.g"], cfg.eps)
-    return linear(silu(linear(h, w[p + "gate.w"])) * linear(h, w[p + "up.w"]), w[p + "down.w"])
+    h = store(rms_norm(x, w[p + "rms2.g"], cfg.eps))
+    return linear(store(silu(linear(h, w[p + "gate.w"])) * linear(h, w[p + "up.w"])), w[p + "down.w"])
 
 
-def lm_head(x, w, cfg):
+def lm_head(x, w, cfg, store=_keep):
     """Final RMSNorm and untied LM head: [n, H] -> [n, vocab] logits."""
-    return linear(rms_norm(x, w["norm.g"], cfg.eps), w["lm_head.w"])
+    return linear(store(rms_norm(x, w["norm.g"], cfg.eps)), w["lm_head.w"])
 
 
 def greedy(logits):
@@ -255,12 +272,18 @@ def greedy(logits):
     return np.argmax(np.asarray(logits), axis=-1).astype(np.int32)
 
 
-def llm_prefill(vis, ids, w, cfg, kv=None, table=None, return_hidden=False):
+def llm_prefill(vis, ids, w, cfg, kv=None, table=None, return_hidden=False, store=_keep):
     """Prefill one request over [visual embeddings ; embedded instruction tokens].
 
     Causal attention spans the whole concatenated sequence; positions are 0..S-1.  If a
     paged cache is given, every layer's rotated K and V are written through ``table``.
     Returns (last-row logits [vocab], next token id) and optionally the final hidden states.
+
+    ``store`` is applied to every tensor a model keeps between operations: the normed input
+    of each projection, the q / k / v projections, the rotated q and k, the attention output,
+    the MLP hidden activation and the final normed row (the residual stream is kept as is).
+    The default keeps exact values; ``bf16_store`` evaluates the same definition as a bf16
+    model stores its tensors.
     """
     vis = np.asarray(vis, F64).reshape(-1, cfg.hidden)
     x = np.concatenate([vis, np.asarray(w["embed"], F64)[np.asarray(ids)]], axis=0)
@@ -268,24 +291,24 @@ def llm_prefill(vis, ids, w, cfg, kv=None, table=None, return_hidden=False):
     pos = np.arange(s)
     for l in range(cfg.layers):
         p = f"l{l}."
-        q, k, v = _qkv(rms_norm(x, w[p + "rms1.g"], cfg.eps), w, l, cfg, pos)
+        q, k, v = _qkv(store(rms_norm(x, w[p + "rms1.g"], cfg.eps)), w, l, cfg, pos, store)
         if kv is not None:
             kv.write(l, table, pos, k, v)
-        att = attention(q, k, v, causal=True, q_pos=pos, k_pos=pos)
+        att = store(attention(q, k, v, causal=True, q_pos=pos, k_pos=pos))
         x = x + linear(att.reshape(s, cfg.n_q * cfg.head_dim), w[p + "o.w"])
-        x = x + _mlp(x, w, l, cfg)
-    logits = lm_head(x[-1:], w, cfg)[0]
+        x = x + _mlp(x, w, l, cfg, store)
+    logits = lm_head(x[-1:], w, cfg, store)[0]
     if return_hidden:
         return logits, int(greedy(logits)), x
     return logits, int(greedy(logits))
 
 
-def llm_decode_step(ids, pos, tables, kv, w, cfg):
+def llm_decode_step(ids, pos, tables, kv, w, cfg, store=_keep):
     """One in-flight-batched decode step.
 
     Sequence b feeds token ids[b] at position pos[b]: its K, V are appended to the paged
     cache, and its single query attends to cached positions 0..pos[b].
-    Returns (logits [B, vocab], next ids [B]).
+    Returns (logits [B, vocab], next ids [B]).  ``store`` as in llm_prefill.
     """
     ids = np.asarray(ids)
     pos = np.asarray(pos)
@@ -293,16 +316,16 @@ def llm_decode_step(ids, pos, tables, kv, w, cfg):
     x = np.asarray(w["embed"], F64)[ids]
     for l in range(cfg.layers):
         p = f"l{l}."
-        h = rms_norm(x, w[p + "rms1.g"], cfg.eps)
+        h = store(rms_norm(x, w[p + "rms1.g"], cfg.eps))
         att = np.empty((bsz, cfg.n_q, cfg.head_dim), F64)
         for b in range(bsz):
-            q, k, v = _qkv(h[b:b + 1], w, l, cfg, pos[b:b + 1])
+            q, k, v = _qkv(h[b:b + 1], w, l, cfg, pos[b:b + 1], store)
             kv.write(l, tables[b], pos[b:b + 1], k, v)
             kc, vc = kv.read(l, tables[b], int(pos[b]) + 1)
             att[b] = attention(q, kc, vc, causal=False)[0]
-        x = x + linear(att.reshape(bsz, cfg.n_q * cfg.head_dim), w[p + "o.w"])
-        x = x + _mlp(x, w, l, cfg)
-    logits = lm_head(x, w, cfg)
+        x = x + linear(store(att).reshape(bsz, cfg.n_q * cfg.head_dim), w[p + "o.w"])
+        x = x + _mlp(x, w, l, cfg, store)
+    logits = lm_head(x, w, cfg, store)
     return logits, greedy(logits)
 
 

@@ -174,6 +174,38 @@ def llm_weights(cfg: LlmConfig, seed: int = 0, names=None) -> dict[str, np.ndarr
     return {k: _draw(k, shapes[k], seed) for k in keys}
 
 
+def _draw_torch(name: str, shape: tuple, seed: int, device):
+    """The same distributions as _draw, drawn on `device` by torch's generator (seeded per tensor
+    name) and rounded to bf16: full-size models are generated in seconds rather than minutes.
+    The values differ from _draw's (another generator); each caller uses one source for both the
+    library and the oracle."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed((int(seed) << 32) | zlib.crc32(name.encode()))
+    std, mean = 0.02, 0.0
+    if name.endswith(".g"):
+        std, mean = 0.2, 1.0
+    elif name.endswith("ln1.b") or name.endswith("ln2.b") or name.endswith("ln.b"):
+        std = 0.2
+    t = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    return (t * std + mean).to(torch.bfloat16)
+
+
+def vit_weights_torch(cfg: VitConfig, seed: int = 0, device="cuda") -> dict:
+    """vit_weights' tensors as bf16 torch tensors drawn on `device`."""
+    return {k: _draw_torch(k, v, seed, device) for k, v in vit_shapes(cfg).items()}
+
+
+def llm_weights_torch(cfg: LlmConfig, seed: int = 0, device="cuda") -> dict:
+    """llm_weights' tensors as bf16 torch tensors drawn on `device`."""
+    return {k: _draw_torch(k, v, seed, device) for k, v in llm_shapes(cfg).items()}
+
+
+def to_host(weights: dict) -> dict[str, np.ndarray]:
+    """Host float32 copies (bf16-exact values) of a dict of bf16 torch tensors."""
+    return {k: v.float().cpu().numpy() for k, v in weights.items()}
+
+
 def image(batch: int, h: int, w: int, seed: int = 1, channels: int = 3) -> np.ndarray:
     """Uniform[0,1) pixels, HWC, rounded to bf16: [batch, h, w, channels] float32."""
     r = _rng(seed, f"image{batch}x{h}x{w}").random(size=(batch, h, w, channels), dtype=np.float32)

@@ -422,3 +422,79 @@ def test_table4_and_offload_table_arithmetic():
     steps = np.diff(o["mem_mb"])
     assert np.allclose(steps, steps[0], atol=0.2)          # one physical layer per extra K
     assert 1 - o["mem_mb"][0] / o["raw_mem_mb"] > 0.9
+
+
+def test_max_rel_err_flags_known_perturbations():
+    """The parity metric itself: max|g - o| / max|o| over one tensor, checked on values whose
+    answer is known by hand, and shown to flag each kind of mistake a parity test must catch."""
+    ref = np.arange(-12.0, 12.0).reshape(4, 6)                 # max |ref| = 12
+    assert vlm.max_rel_err(ref, ref) == 0.0
+    got = ref.copy()
+    got[1, 3] += 0.3                                            # one element off by 0.3
+    assert vlm.max_rel_err(got, ref) == pytest.approx(0.3 / 12.0, rel=1e-12)
+    assert vlm.max_rel_err(3.5 * got, 3.5 * ref) == pytest.approx(0.3 / 12.0, rel=1e-12)   # scale-free
+    assert vlm.max_rel_err(np.zeros(3), np.zeros(3)) == 0.0    # an all-zero reference is absolute
+    assert vlm.max_rel_err(np.full(3, 0.5), np.zeros(3)) == 0.5
+    # the 2e-2 bound: a 2.5% error in the largest element fails it, a 1% one passes
+    big = ref.copy()
+    big[0, 0] *= 1.025
+    small = ref.copy()
+    small[0, 0] *= 1.01
+    assert vlm.max_rel_err(big, ref) > 2e-2 > vlm.max_rel_err(small, ref)
+    # a flipped sign, a transposed operand, a dropped term and a shifted index are all far above it
+    rng = np.random.default_rng(0)
+    a = rng.standard_normal((8, 8))
+    b = rng.standard_normal((8, 8))
+    flipped = a.copy()
+    flipped[2, 5] = -flipped[2, 5]
+    assert vlm.max_rel_err(flipped, a) > 2e-2 or a[2, 5] == 0
+    assert vlm.max_rel_err(a.T @ b, a @ b) > 2e-2
+    assert vlm.max_rel_err(a @ b, a @ b + 0.1 * b) > 2e-2
+    assert vlm.max_rel_err(np.roll(a, 1, axis=0), a) > 2e-2
+    # NaN anywhere in the output is never within tolerance
+    nan = a.copy()
+    nan[3, 3] = np.nan
+    assert not vlm.max_rel_err(nan, a) < 2e-2
+
+
+def test_bf16_store_rounding():
+    """bf16_store against torch's float32 -> bfloat16 conversion (an independent implementation of
+    round-to-nearest-even) and against hand-worked ties."""
+    import torch
+    rng = np.random.default_rng(5)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-30, 30, 20000),
+                        [0.0, -0.0, 1e-40, -3e-39, np.inf, -np.inf, 3.3895e38, 1.0, -2.5]]).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.bfloat16).float().numpy().astype(np.float64)
+    got = vlm.bf16_store(x)
+    assert np.array_equal(got, want)
+    one = 1.0
+    assert vlm.bf16_store(one + 2.0 ** -8) == 1.0                   # halfway, to the even neighbour 1
+    assert vlm.bf16_store(one + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6    # halfway, to the even neighbour above
+    assert vlm.bf16_store(one + 2.0 ** -8 + 2.0 ** -20) == 1.0 + 2.0 ** -7   # just past halfway: up
+    assert np.isnan(vlm.bf16_store(np.nan))
+    assert np.array_equal(vlm.bf16_store(got), got)                  # idempotent
+
+
+def test_bf16_store_points_in_the_llm():
+    """The stored tensors of the bf16-storage reading: per layer the normed input, the q / k / v
+    projections, the rotated q and k, the attention output, the MLP's normed input and hidden
+    activation; then the final normed row (prefill: last row only)."""
+    cfg = synth.TINY_LLM
+    w = synth.llm_weights(cfg, seed=0)
+    seen = []
+
+    def store(t):
+        seen.append(np.shape(t))
+        return t
+    vis = synth.vision_embeds(8, cfg.hidden)
+    ids = synth.text_ids(5, cfg.vocab)
+    s, H, d = 13, cfg.hidden, cfg.head_dim
+    exact = vlm.llm_prefill(vis, ids, w, cfg)[0]
+    got = vlm.llm_prefill(vis, ids, w, cfg, store=store)[0]
+    assert np.array_equal(got, exact)                                # recording changes nothing
+    per_layer = [(s, H), (s, cfg.n_q * d), (s, cfg.n_q, d), (s, cfg.n_kv * d), (s, cfg.n_kv, d), (s, cfg.n_kv * d),
+                 (s, cfg.n_q, d), (s, H), (s, cfg.inter)]
+    assert seen == per_layer * cfg.layers + [(1, H)]
+    # bf16 storage moves the logits by a bf16-sized amount, no more
+    rounded = vlm.llm_prefill(vis, ids, w, cfg, store=vlm.bf16_store)[0]
+    assert 1e-4 < vlm.max_rel_err(rounded, exact) < 2e-2
