@@ -199,6 +199,23 @@ int nova_llm_decode(const nova_llm* llm, const int32_t* ids, const int32_t* pos,
                     int max_blocks, int batch, int max_ctx, const nova_kv* kv, int32_t* next_ids, float* logits,
                     void* ws, size_t ws_bytes, nova_stream_t stream);
 
+/* Allocation-free decode step, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the same step as
+ * nova_llm_decode, same arguments and results, with its workspace (activations, split-K partial
+ * sums, arrival counters, attention split partials) taken from a library-owned static device
+ * array of NOVA_DECODE_SCRATCH_BYTES bytes, which each GPU the library runs on holds until the
+ * process ends.  Calls no hipMalloc, hipFree or other allocating routine.  The step clears what
+ * must start at zero (argmax keys, arrival counters) in its own first kernel; the array keeps the
+ * last call's contents otherwise.  Every call on one GPU uses that GPU's single array: calls that
+ * overlap in time on one GPU (two streams, two threads) race on it and give wrong results, so
+ * the caller serialises them.  A step whose workspace (nova_llm_decode_workspace_bytes) exceeds
+ * NOVA_DECODE_SCRATCH_BYTES returns NOVA_ENOSPACE and launches nothing; the 28-layer 3584-wide
+ * decoder at batch 32 needs about 9 MB. */
+#define NOVA_DECODE_SCRATCH_BYTES (32u << 20)
+int nova_llm_decode_noalloc(const nova_llm* llm, const int32_t* ids, const int32_t* pos, const int32_t* block_tables,
+                            int max_blocks, int batch, int max_ctx, const nova_kv* kv, int32_t* next_ids,
+                            float* logits, nova_stream_t stream);
+
 /* ------------------------------------------------------------------ CU partitions (Sec. 3.2.2)
  * gfx950 deals a kernel's workgroups round-robin over its 8 XCDs, and a CU-mask bit i selects
  * CU slot i/32 of shader engine (i/8)%4 of XCD i%8.  A partition therefore never confines a

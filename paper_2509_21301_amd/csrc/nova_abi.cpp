@@ -114,6 +114,10 @@ inline bool aligned(const void* p) { return ((uintptr_t)p & 255) == 0; }
     if (rc_ != NOVA_OK) return rc_;                                                \
   } while (0)
 
+namespace {
+int scratch_for_current_device(void** out);
+}
+
 extern "C" int nova_init(int device) {
   int n = 0;
   HIP_TRY(hipGetDeviceCount(&n));
@@ -123,7 +127,8 @@ extern "C" int nova_init(int device) {
   HIP_TRY(hipGetDeviceProperties(&prop, device));
   g.device = device;
   g.cus = prop.multiProcessorCount;
-  return NOVA_OK;
+  void* scr = nullptr;   // the allocation-free decode's scratch address on this device
+  return scratch_for_current_device(&scr);
 }
 
 extern "C" void nova_shutdown(void) {
@@ -849,21 +854,79 @@ extern "C" int nova_llm_prefill(const nova_llm* m, const void* vis, int n_vis, c
              : llm_prefill_t<bf16_t>(m, (const bf16_t*)vis, n_vis, ids, n_text, table, kv, next_id, logits, ws, s);
 }
 
-extern "C" int nova_llm_decode(const nova_llm* m, const int32_t* ids, const int32_t* pos, const int32_t* tables,
-                               int max_blocks, int batch, int max_ctx, const nova_kv* kv, int32_t* next_ids,
-                               float* logits, void* ws, size_t ws_bytes, nova_stream_t stream) {
+namespace {
+// Argument checks shared by the two decode entry points (everything but the workspace).
+int check_decode_args(const nova_llm* m, const int32_t* ids, const int32_t* pos, const int32_t* tables, int max_blocks,
+                      int batch, int max_ctx, const nova_kv* kv, const int32_t* next_ids) {
   if (!m || !kv) return fail(NOVA_EINVAL, "null model or kv");
   if (batch <= 0 || batch > 32) return fail(NOVA_EINVAL, "batch %d outside 1..32", batch);
-  if (!ids || !pos || !tables || !next_ids || !ws || !aligned(ws)) return fail(NOVA_EINVAL, "null or misaligned pointer");
+  if (!ids || !pos || !tables || !next_ids) return fail(NOVA_EINVAL, "null pointer");
   if (max_ctx <= 0 || max_blocks <= 0) return fail(NOVA_EINVAL, "max_ctx and max_blocks must be positive");
   if ((max_ctx + m->d.cfg.block - 1) / m->d.cfg.block > max_blocks) return fail(NOVA_ENOKV, "max_ctx exceeds the block table width");
   if (!kv->k || !kv->v || kv->num_blocks <= 0) return fail(NOVA_EINVAL, "invalid kv pool");
-  const size_t need = nova_llm_decode_workspace_bytes(m, batch, max_ctx);
-  if (ws_bytes < need) return fail(NOVA_ENOSPACE, "workspace %zu < required %zu bytes", ws_bytes, need);
-  hipStream_t s = (hipStream_t)stream;
+  return NOVA_OK;
+}
+
+int decode_dispatch(const nova_llm* m, const int32_t* ids, const int32_t* pos, const int32_t* tables, int max_blocks,
+                    int batch, int max_ctx, const nova_kv* kv, int32_t* next_ids, float* logits, void* ws,
+                    hipStream_t s) {
   return m->d.cfg.act == NOVA_ACT_F32
              ? llm_decode_t<float>(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids, logits, ws, s)
              : llm_decode_t<bf16_t>(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids, logits, ws, s);
+}
+}  // namespace
+
+extern "C" int nova_llm_decode(const nova_llm* m, const int32_t* ids, const int32_t* pos, const int32_t* tables,
+                               int max_blocks, int batch, int max_ctx, const nova_kv* kv, int32_t* next_ids,
+                               float* logits, void* ws, size_t ws_bytes, nova_stream_t stream) {
+  if (int rc = check_decode_args(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids)) return rc;
+  if (!ws || !aligned(ws)) return fail(NOVA_EINVAL, "null or misaligned workspace");
+  const size_t need = nova_llm_decode_workspace_bytes(m, batch, max_ctx);
+  if (ws_bytes < need) return fail(NOVA_ENOSPACE, "workspace %zu < required %zu bytes", ws_bytes, need);
+  return decode_dispatch(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids, logits, ws, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ allocation-free decode
+// The decode workspace of nova_llm_decode_noalloc: one static device array, which every GPU the
+// library runs on holds at its own address until the process ends.  Host code never passes the
+// array's name to a kernel or a copy (on the host it only stands in for the symbol); it uses the
+// device address that hipGetSymbolAddress returns, once per device, with that device current.
+static __device__ __align__(256) unsigned char scratch[NOVA_DECODE_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (resolved on first use per device).
+int scratch_for_current_device(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(NOVA_EUNSUPPORTED, "device %d beyond the scratch table", dev);
+  std::lock_guard<std::mutex> lk(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return fail(NOVA_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    scratch_ptr[dev] = ptr;
+  }
+  *out = scratch_ptr[dev];
+  return NOVA_OK;
+}
+}  // namespace
+
+extern "C" int nova_llm_decode_noalloc(const nova_llm* m, const int32_t* ids, const int32_t* pos,
+                                       const int32_t* tables, int max_blocks, int batch, int max_ctx,
+                                       const nova_kv* kv, int32_t* next_ids, float* logits, nova_stream_t stream) {
+  if (int rc = check_decode_args(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids)) return rc;
+  const size_t need = nova_llm_decode_workspace_bytes(m, batch, max_ctx);
+  if (need > (size_t)NOVA_DECODE_SCRATCH_BYTES)
+    return fail(NOVA_ENOSPACE, "decode step needs %zu bytes of workspace, above the %zu-byte static scratch "
+                               "(use nova_llm_decode with a caller workspace)", need, (size_t)NOVA_DECODE_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if (int rc = scratch_for_current_device(&ws)) return rc;
+  // the step clears what must start at zero (argmax keys, arrival counters) in its first kernel
+  return decode_dispatch(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids, logits, ws, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ CU partitions

@@ -80,6 +80,8 @@ _SIG = {
                                    C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "nova_llm_decode": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_int,
                                   C.POINTER(KvC), C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "nova_llm_decode_noalloc": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_int,
+                                          C.POINTER(KvC), C.c_void_p, C.c_void_p, C.c_void_p]),
     "nova_make_cu_mask": (C.c_int, [C.c_int, C.c_int, C.POINTER(C.c_uint32)]),
     "nova_set_stage_partition": (C.c_int, [C.c_int, C.POINTER(C.c_uint32), C.c_int, C.POINTER(C.c_void_p)]),
     "nova_cu_probe": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int]),
@@ -389,6 +391,13 @@ class Llm:
         _check(lib.nova_llm_decode(self.h, _ptr(ids), _ptr(pos), _ptr(tables), tables.shape[1], b, max_ctx,
                                    C.byref(kv.c), _ptr(next_ids), _ptr(logits), _ptr(ws), ws.numel(),
                                    _stream(stream)))
+        return next_ids
+
+    def decode_noalloc(self, ids, pos, tables, kv, max_ctx, next_ids, logits=None, stream=None):
+        """The same step with the library's static scratch as workspace (no allocation in the
+        library; outputs are the caller's)."""
+        _check(lib.nova_llm_decode_noalloc(self.h, _ptr(ids), _ptr(pos), _ptr(tables), tables.shape[1], ids.shape[0],
+                                           max_ctx, C.byref(kv.c), _ptr(next_ids), _ptr(logits), _stream(stream)))
         return next_ids
 
     def __del__(self):
