@@ -192,16 +192,23 @@ class Stages:
 
 class ServingSetup:
     """The screenshot workload: a 1092x2408 image (13416 patches, 3354 merged tokens) through the
-    same 32-layer encoder (its own position table), prompts of 3354 + 150..300 tokens."""
+    same 32-layer encoder (its own position table), prompts of 3354 + 150..300 tokens.  With
+    n_slots > 0 the encoder's layers stay in pinned host memory and stream through that many
+    device slots (Sec. 3.5); kv_blocks sizes the paged KV pool."""
 
-    def __init__(self, nova, torch, synth, st):
+    def __init__(self, nova, torch, synth, st, n_slots=0, kv_blocks=12000):
         self.nova, self.torch, self.synth, self.st = nova, torch, synth, st
         cfg = synth.VIT_SCREEN
         gen = torch.Generator(device="cuda")
         gen.manual_seed(11)
         (eo, eb), _, _ = nova.vit_layouts(cfg)
         emb = random_blob(eb, eo, [], "cuda", gen)
-        self.vit = nova.Vit(cfg, None, blobs=(emb, st.vit.layers, st.vit.head, st.vit.layer_bytes))
+        layers = st.vit.layers
+        if n_slots > 0:
+            layers = torch.empty(st.vit.layers.numel(), dtype=torch.bfloat16, pin_memory=True)
+            layers.copy_(st.vit.layers)
+        self.n_slots, self.kv_blocks = n_slots, kv_blocks
+        self.vit = nova.Vit(cfg, None, blobs=(emb, layers, st.vit.head, st.vit.layer_bytes), n_slots=n_slots)
         img = synth.image(1, cfg.image_h, cfg.image_w, seed=21)
         self.pixels = torch.from_numpy(img).to("cuda", torch.bfloat16).contiguous()
         self.vis = torch.empty(self.vit.out_shape(1), dtype=torch.bfloat16, device="cuda")
@@ -209,7 +216,7 @@ class ServingSetup:
         self.ids = torch.from_numpy(synth.text_ids(nt, st.lc.vocab, seed=22)).cuda()
         s = cfg.n_out + nt
         self.max_blocks = (cfg.n_out + 300 + 48 + 15) // 16
-        tables, pool = synth.block_tables([s], 16, seed=23, num_blocks=12000)
+        tables, pool = synth.block_tables([s], 16, seed=23, num_blocks=kv_blocks)
         self.kv = nova.KvPool(st.llm, pool)
         self.table = torch.from_numpy(tables[0]).cuda()
 
@@ -219,10 +226,117 @@ class ServingSetup:
     def prefill(self, stream):
         self.st.llm.prefill(self.vis[0], self.ids, self.table, self.kv, stream=stream)
 
-    def serve(self, kw, trace):
+    def serve(self, kw, trace, keep_log=False):
         from paper_2509_21301_amd import serve
         srv = serve.Server(self.vit, self.st.llm, self.kv, self.pixels, max_blocks=self.max_blocks, **kw)
-        return srv.run(trace)
+        res = srv.run(trace)
+        if keep_log and srv.partition_log:
+            t0 = min(r.t_arrive for r in trace)
+            res["partition_timeline"] = [[round((t - t0) * 1e3, 2), st, cus] for t, st, cus in srv.partition_log]
+            res["arrivals_ms"] = [round(r.arrival * 1e3, 1) for r in trace]
+        return res
+
+
+# ----------------------------------------------------------------------------- serving runs
+def serving_modes(sched, curves, out_len, rate, adaptive):
+    """The systems compared on one trace: Nova at the rate's Pareto point (Eq. 1 + Eq. 6) and with
+    the Eq. 5 adaptation (parameters from adaptive_params), time slicing decode-first and
+    prefill-first, the PF-Limit baseline (prefill-first, decode once more than 5 wait; Sec. 5.1),
+    and unpartitioned streams (Multi-Stream)."""
+    rv, rp, _ = sched.best_under_load(sched.on_granule(curves), out_len, rate)
+    a = adaptive
+    return [("nova_rate_static", dict(mode="nova", decode_cus=(rv, rp))),
+            ("nova_adaptive", dict(mode="nova", decode_cus=(a["sm_op_v"], a["sm_op_p"]),
+                                   alpha=(a["alpha_v"], a["alpha_p"]), minimum=a["sm_min"])),
+            ("time_sliced_decode_first", dict(mode="time_sliced", slice_order="decode_first")),
+            ("time_sliced_prefill_first", dict(mode="time_sliced", slice_order="prefill_first")),
+            ("pf_limit", dict(mode="time_sliced", slice_order="prefill_first", decode_limit=5)),
+            ("multi_stream", dict(mode="multi_stream"))]
+
+
+def run_serving(serve, sched, srv, curves, out_len, rates, seeds, window, modes=None, timeline_at=None):
+    """Every mode on the same Poisson traces (rate x seed); per (mode, rate) the mean and spread
+    over seeds, the better of the two time-sliced orders, and Eq. 6 beside the measured wait."""
+    grid = sorted(set([0.25, 0.5, 1, 1.5, 2, 3, 4, 5, 6, 7, 8] + list(rates)))
+    adaptive = sched.adaptive_params(curves, out_len, grid)
+    log(f"adaptive Eq. 5 parameters: SM_op {adaptive['sm_op_v']}/{adaptive['sm_op_p']}, alpha "
+        f"{adaptive['alpha_v']}/{adaptive['alpha_p']}, SM_min {adaptive['sm_min']}")
+    runs = []
+    for rate in rates:
+        for seed in seeds:
+            for mode, kw in serving_modes(sched, curves, out_len, rate, adaptive):
+                if modes and mode not in modes:
+                    continue
+                trace = serve.poisson_trace(rate, window, seed=seed)
+                res = srv.serve(kw, trace, keep_log=(timeline_at == (rate, seed) and mode == "nova_adaptive"))
+                res.update({"mode": mode, "rate_req_s": rate, "seed": seed, "window_s": window,
+                            "decode_cus": list(kw.get("decode_cus", (256, 256)))})
+                runs.append(res)
+                log(f"serve {mode:26s} rate {rate} seed {seed}: max E2E {res['max_e2e_s']:.3f} s, avg "
+                    f"{res['avg_e2e_s']:.3f} s, avg TBT {res['avg_tbt_ms']:.1f} ms, decode batch "
+                    f"{res['avg_decode_batch']:.2f}, vision wait {res['avg_queue_wait_s']:.3f} s (Eq. 6: "
+                    f"{res['eq6_predicted_wait_s']})")
+    summary = []
+    for rate in rates:
+        for mode in dict.fromkeys(r["mode"] for r in runs):
+            rs = [r for r in runs if r["mode"] == mode and r["rate_req_s"] == rate]
+            if not rs:
+                continue
+            row = {"mode": mode, "rate_req_s": rate, "seeds": len(rs), "requests": int(sum(r["requests"] for r in rs))}
+            for k in ("max_e2e_s", "avg_e2e_s", "avg_ttft_s", "avg_tbt_ms", "avg_decode_batch", "throughput_req_s",
+                      "avg_queue_wait_s"):
+                v = np.array([r[k] for r in rs], float)
+                row[k] = round(float(v.mean()), 4)
+                row[k + "_std"] = round(float(v.std()), 4)
+            # Eq. 6 over the pooled service times of all seeds
+            t = np.array([r["mean_service_s"] for r in rs])
+            t2 = np.array([r["mean_service2_s2"] for r in rs])
+            w = sched.mg1_wait(rate, float(t.mean()), float(t2.mean()))
+            row["eq6_predicted_wait_s"] = None if w == float("inf") else round(w, 4)
+            row["utilization"] = round(rate * float(t.mean()), 3)
+            summary.append(row)
+        sl = [r for r in summary if r["rate_req_s"] == rate and r["mode"] in ("time_sliced_decode_first",
+                                                                               "time_sliced_prefill_first")]
+        if sl:
+            best = min(sl, key=lambda r: r["max_e2e_s"])
+            summary.append(dict(best, mode="time_sliced_best", chosen=best["mode"]))
+    return {"adaptive_params": adaptive, "summary": summary, "runs": runs}
+
+
+
+
+def measure_corun(nova, torch, st, srv):
+    """Decode (batch 8) on P CUs beside the screenshot encode or a 3.6k-token prefill on the other
+    256 - P, for P = 32..224: the co-run curves the Eq. 3 search consumes."""
+    corun = []
+    for other in ("encode", "prefill"):
+        for p in [32, 64, 96, 128, 160, 192, 224]:
+            s_d = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(p, 0))
+            so = nova.set_stage_partition(nova.STAGE_ENCODE if other == "encode" else nova.STAGE_PREFILL,
+                                          nova.make_cu_mask(256 - p, p // 8))
+            run_other = (lambda: srv.encode(so)) if other == "encode" else (lambda: srv.prefill(so))
+            t_o = time_passes(torch, run_other, 1, so)
+            t_d = time_passes(torch, lambda: st.decode(8, stream=s_d), 5, s_d)
+            n_dec = max(4, int(t_o / max(t_d, 1e-3)) + 2)
+            torch.cuda.synchronize()
+            eo0, eo1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ed0, ed1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            eo0.record(so)
+            run_other()
+            eo1.record(so)
+            ed0.record(s_d)
+            for _ in range(n_dec):
+                st.decode(8, stream=s_d)
+            ed1.record(s_d)
+            torch.cuda.synchronize()
+            t_oc = eo0.elapsed_time(eo1)
+            t_dc = ed0.elapsed_time(ed1) / n_dec
+            corun.append({"pair": f"decode+{other}", "decode_cus": p, "other_cus": 256 - p,
+                          f"{other}_ms_solo_on_partition": round(t_o, 3), f"{other}_ms_corun": round(t_oc, 3),
+                          "decode_step_ms_solo_on_partition": round(t_d, 3), "decode_step_ms_corun": round(t_dc, 3)})
+            log(f"co-run decode {p} / {other} {256 - p}: {other} {t_oc:.2f} ms (solo {t_o:.2f}), "
+                f"decode step {t_dc:.3f} ms (solo {t_d:.3f})")
+    return corun
 
 
 # ----------------------------------------------------------------------------- offload (Sec. 3.5)
@@ -283,18 +397,44 @@ def measure_offload(nova, torch, st, srv, slots=(2, 3, 4, 5)):
 
 
 # ----------------------------------------------------------------------------- CPU baseline
-def cpu_baseline(synth):
-    """The oracle, as is, on one image's worth of encoder layers at the real shape (2 of 32
-    layers plus the adapter), extrapolated to a full 32-layer pass."""
-    from oracle import vlm
+def _host_info():
+    """Threads the oracle's BLAS uses, the BLAS library, and the host CPU model."""
+    threads, blas = os.cpu_count() or 1, "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        info = [p for p in threadpool_info() if p.get("user_api") == "blas"] or threadpool_info()
+        if info:
+            threads = max(p.get("num_threads", 1) for p in info)
+            blas = ", ".join(sorted({f"{p.get('internal_api', '?')} {p.get('version', '')}".strip() for p in info}))
     except Exception:
-        threads = os.cpu_count() or 1
+        pass
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return int(threads), blas, model
+
+
+def cpu_baseline(synth):
+    """The oracle, as is (float64 NumPy), on bounded samples of each stage at the real shapes:
+    * encode: one 1008x1008 image's patch embedding, 2 of the 32 encoder layers and the adapter,
+      extrapolated to a full pass (the headline unit, patches/s);
+    * prefill: one of the 28 decoder layers over the 1500-token prompt plus the LM head on a
+      1/16 slice of the vocabulary, extrapolated to 28 layers and the full head (tok/s);
+    * decode: one batch-1 step through one layer at a 1500-token context, and the head slice,
+      extrapolated the same way (tok/s);
+    * the tiny stack end to end (encode, 96-token prefill, 16 greedy decode steps)."""
+    import dataclasses
+    from oracle import vlm
+    threads, blas, model = _host_info()
+    out = {}
+    # encode
     cfg = synth.VIT_1008
-    names = ["patch.w", "patch.b", "pos", "merge.ln.g", "merge.ln.b", "merge.w", "merge.b"]
-    names += synth.vit_layer_names(0)
+    names = ["patch.w", "patch.b", "pos", "merge.ln.g", "merge.ln.b", "merge.w", "merge.b"] + synth.vit_layer_names(0)
     w = synth.vit_weights(cfg, seed=0, names=names)
     img = synth.image(1, cfg.image_h, cfg.image_w, seed=1)[0]
     t0 = time.perf_counter()
@@ -309,10 +449,57 @@ def cpu_baseline(synth):
     vlm.merge_adapter(x, w, cfg)
     t_merge = time.perf_counter() - t0
     t_img = t_embed + cfg.layers * t_layer + t_merge
-    return {"value": round(cfg.n_patches / t_img, 2), "unit": "patches/s", "cores": int(threads), "kind": "oracle",
+    del w, x
+    # prefill and decode: one real-width layer, the LM head on a vocabulary slice
+    lc = synth.LLM_28
+    vs = lc.vocab // 16
+    l1 = dataclasses.replace(lc, layers=1, vocab=vs)
+    wl = synth.llm_weights(l1, seed=0)
+    nv, nt = synth.LLM_VISION_TOKENS, synth.LLM_TEXT_TOKENS
+    s = nv + nt
+    xs = np.concatenate([synth.vision_embeds(nv, lc.hidden), wl["embed"][synth.text_ids(nt, vs)]], 0)
+    t0 = time.perf_counter()
+    h, _, _ = vlm.llm_layer_rows(xs, wl, 0, l1, np.arange(s))
+    t_pre_layer = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    vlm.lm_head(h[-1:], wl, l1)
+    t_head = (time.perf_counter() - t0) * (lc.vocab / vs)
+    t_prefill = lc.layers * t_pre_layer + t_head
+    tables, pool = synth.block_tables([s + 1], lc.block, seed=5)
+    kv = vlm.PagedKV(1, pool, lc.n_kv, lc.block, lc.head_dim)
+    rng = np.random.default_rng(0)
+    kv.k[:] = rng.standard_normal(kv.k.shape)
+    kv.v[:] = rng.standard_normal(kv.v.shape)
+    t0 = time.perf_counter()
+    vlm.llm_decode_step(np.array([5]), np.array([s]), tables, kv, wl, l1)
+    t_dec1 = time.perf_counter() - t0
+    t_decode = lc.layers * t_dec1 + t_head          # the slice's head time is inside t_dec1; upper bound
+    del wl, kv
+    # tiny stack end to end
+    tv, tl = synth.TINY_VIT, synth.TINY_LLM
+    wv, wt = synth.vit_weights(tv, 0), synth.llm_weights(tl, 0)
+    timg = synth.image(1, tv.image_h, tv.image_w, seed=1)[0]
+    tids = synth.text_ids(synth.TINY_TEXT, tl.vocab, seed=2)
+    t0 = time.perf_counter()
+    vis = vlm.vit_encode(timg, wv, tv)
+    ts = vis.shape[0] + synth.TINY_TEXT
+    ttab, tpool = synth.block_tables([ts + synth.TINY_DECODE_STEPS], tl.block, seed=5)
+    tkv = vlm.PagedKV(tl.layers, tpool, tl.n_kv, tl.block, tl.head_dim)
+    _, tok = vlm.llm_prefill(vis, tids, wt, tl, kv=tkv, table=ttab[0])
+    for t in range(synth.TINY_DECODE_STEPS):
+        tok = int(vlm.llm_decode_step(np.array([tok]), np.array([ts + t]), ttab, tkv, wt, tl)[1][0])
+    t_tiny = time.perf_counter() - t0
+    return {"value": round(cfg.n_patches / t_img, 2), "unit": "patches/s", "cores": threads, "kind": "oracle",
+            "precision": "float64", "blas": blas, "cpu_model": model,
             "sample": f"1 image of {cfg.image_h}x{cfg.image_w} ({cfg.n_patches} patches): patch embed, "
                       f"{layers_timed} of {cfg.layers} encoder layers timed (float64 NumPy), adapter; "
-                      f"full pass extrapolated as embed + {cfg.layers} x layer + adapter = {t_img:.1f} s"}
+                      f"full pass extrapolated as embed + {cfg.layers} x layer + adapter = {t_img:.1f} s",
+            "stages": {"encode_image_s": round(t_img, 2),
+                       "prefill_s1500_s": round(t_prefill, 2), "prefill_tok_per_s": round(s / t_prefill, 2),
+                       "decode_b1_step_s": round(t_decode, 3), "decode_b1_tok_per_s": round(1 / t_decode, 3),
+                       "tiny_stack_end_to_end_s": round(t_tiny, 3),
+                       "note": "prefill and decode: 1 of 28 layers timed and the LM head on 1/16 of the "
+                               "vocabulary, extrapolated to 28 layers and the full head"}}
 
 
 # ----------------------------------------------------------------------------- main
@@ -326,6 +513,13 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--rates", type=float, nargs="+", default=[2.0, 4.0], help="request rates (req/s) of the serving runs")
     ap.add_argument("--window", type=float, default=10.0, help="arrival window (s) of each serving run")
+    ap.add_argument("--seeds", type=int, nargs="+", default=[3], help="trace seeds of the serving runs")
+    ap.add_argument("--serving-sweep", action="store_true",
+                    help="only the co-run curves and the serving runs over --rates x --seeds (prints their JSON)")
+    ap.add_argument("--hbm-budget", action="store_true",
+                    help="only the serving runs under an HBM budget: encoder layers offloaded (K = 2 slots), "
+                         "KV pool capped at 40 GB, batch-32 decode (prints their JSON)")
+    ap.add_argument("--modes", nargs="+", default=None, help="restrict the serving modes")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
     ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32", "copy", "offload"],
                     help="run only this stage in a loop of --steps passes (for rocprofv3); 'copy' is a plain "
@@ -354,6 +548,37 @@ def main():
     B = args.batch
     stream = torch.cuda.current_stream()
 
+    if args.serving_sweep or args.hbm_budget:
+        out_len = 32.0
+        srv = ServingSetup(nova, torch, synth, st)
+        corun = measure_corun(nova, torch, st, srv)
+        curves = sched.StageCurves.from_corun(corun)
+        res = {"corun": corun}
+        if args.serving_sweep:
+            sv = run_serving(serve, sched, srv, curves, out_len, args.rates, args.seeds, args.window, modes=args.modes,
+                             timeline_at=(args.rates[-1], args.seeds[0]))
+            res["serving_sweep"] = sv
+        if args.hbm_budget:
+            # Sec. 3.5 inside serving: 40 GB of KV blocks (43,596 of 917,504 bytes), the encoder's 32
+            # layers streamed through 2 device slots, requests at --rates with decode batches up to 32
+            kv_blocks = int(40e9 // (lc.layers * 2 * lc.n_kv * lc.block * lc.head_dim * 2))
+            del srv
+            torch.cuda.empty_cache()
+            off = ServingSetup(nova, torch, synth, st, n_slots=2, kv_blocks=kv_blocks)
+            sv = run_serving(serve, sched, off, curves, out_len, args.rates, args.seeds, args.window, modes=args.modes)
+            sv["kv_blocks"], sv["kv_gb"] = kv_blocks, round(off.kv.k.numel() * 4 / 1e9, 2)
+            sv["encoder_device_mb"] = round(2 * st.vit.layer_bytes / 1e6, 1)
+            res["hbm_budget"] = sv
+            # the same traces with the encoder resident, for the offload overhead inside serving
+            del off
+            torch.cuda.empty_cache()
+            res_srv = ServingSetup(nova, torch, synth, st, kv_blocks=kv_blocks)
+            res["hbm_budget_resident_encoder"] = run_serving(
+                serve, sched, res_srv, curves, out_len, args.rates, args.seeds, args.window,
+                modes=["nova_adaptive", "nova_rate_static"])
+        print(json.dumps(res), flush=True)
+        return
+
     if args.profile_stage == "offload":
         print(json.dumps(measure_offload(nova, torch, st, ServingSetup(nova, torch, synth, st))), flush=True)
         return
@@ -365,13 +590,9 @@ def main():
         log(f"{args.profile_stage}: {ms:.3f} ms per pass")
         return
 
-    # ---------------- headline: encode, batch B, all CUs
+    # ---------------- headline: encode, batch B, all CUs (no per-kernel events in the timed loop)
     for _ in range(args.warmup):
         st.encode()
-    torch.cuda.synchronize()
-    nova.timing_enable(True)
-    for k in nova.KIND_NAMES:
-        nova.timing_read(k)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0 = torch.cuda.Event(enable_timing=True)
@@ -383,27 +604,38 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1)
-    kinds = {nova.KIND_NAMES[k]: nova.timing_read(k) for k in nova.KIND_NAMES}
-    nova.timing_enable(False)
     ms_step = ms / args.steps
     value = B * vc.n_patches * args.steps / (ms / 1e3)
     gemm_f, attn_f = vit_flops(vc, B)
     log(f"encode batch {B}: {ms_step:.2f} ms/pass, {value:.0f} patches/s, "
         f"{(gemm_f + attn_f) / (ms_step / 1e3) / 1e12:.1f} TFLOP/s overall (wall {wall:.2f}s)")
+    # kernel families: the same passes again with every family launch bracketed by HIP events that
+    # the library records on the stream it launches on
+    fam_steps = max(2, args.steps // 2)
+    nova.timing_enable(True)
+    for k in nova.KIND_NAMES:
+        nova.timing_read(k)
+    for _ in range(fam_steps):
+        st.encode()
+    torch.cuda.synchronize()
+    kinds = {nova.KIND_NAMES[k]: nova.timing_read(k) for k in nova.KIND_NAMES}
+    nova.timing_enable(False)
     for nm, (t, n) in kinds.items():
-        log(f"  {nm:18s} {t / args.steps:9.3f} ms/pass  {n / args.steps:6.1f} launches/pass")
+        log(f"  {nm:18s} {t / fam_steps:9.3f} ms/pass  {n / fam_steps:6.1f} launches/pass")
     # dominant kernel family of the pass and its roofline position
     fam_flops = {"gemm": gemm_f, "attention": attn_f}
     dom = max(fam_flops, key=lambda f: kinds[f][0])
     t_dom, n_dom = kinds[dom]
-    flops_per_launch = fam_flops[dom] * args.steps / max(n_dom, 1)
+    flops_per_launch = fam_flops[dom] * fam_steps / max(n_dom, 1)
     achieved = flops_per_launch / ((t_dom / max(n_dom, 1)) / 1e3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
                 "traffic": gemm_traffic() if dom == "gemm" else None,
                 "avg_launch_ms": round(t_dom / max(n_dom, 1), 4),
                 "flops_per_launch": flops_per_launch,
-                "other_kernels": {f: round(fam_flops[f] * args.steps / kinds[f][0] / 1e9, 1)
+                "family_passes": fam_steps,
+                "family_ms_per_pass": {f: round(kinds[f][0] / fam_steps, 3) for f in kinds},
+                "other_kernels": {f: round(fam_flops[f] * fam_steps / kinds[f][0] / 1e9, 1)
                                   for f in fam_flops if f != dom and kinds[f][0] > 0}}
 
     result = {
@@ -463,34 +695,7 @@ def main():
         # co-run on the serving shapes: decode (batch 8) on P CUs with the screenshot encode or a
         # 3.5k-token prefill on the other 256 - P; these are the curves the Eq. 3 search consumes
         srv = ServingSetup(nova, torch, synth, st)
-        corun = []
-        for other in ("encode", "prefill"):
-            for p in [32, 64, 96, 128, 160, 192, 224]:
-                s_d = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(p, 0))
-                so = nova.set_stage_partition(nova.STAGE_ENCODE if other == "encode" else nova.STAGE_PREFILL,
-                                              nova.make_cu_mask(256 - p, p // 8))
-                run_other = (lambda: srv.encode(so)) if other == "encode" else (lambda: srv.prefill(so))
-                t_o = time_passes(torch, run_other, 1, so)
-                t_d = time_passes(torch, lambda: st.decode(8, stream=s_d), 5, s_d)
-                n_dec = max(4, int(t_o / max(t_d, 1e-3)) + 2)
-                torch.cuda.synchronize()
-                eo0, eo1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                ed0, ed1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                eo0.record(so)
-                run_other()
-                eo1.record(so)
-                ed0.record(s_d)
-                for _ in range(n_dec):
-                    st.decode(8, stream=s_d)
-                ed1.record(s_d)
-                torch.cuda.synchronize()
-                t_oc = eo0.elapsed_time(eo1)
-                t_dc = ed0.elapsed_time(ed1) / n_dec
-                corun.append({"pair": f"decode+{other}", "decode_cus": p, "other_cus": 256 - p,
-                              f"{other}_ms_solo_on_partition": round(t_o, 3), f"{other}_ms_corun": round(t_oc, 3),
-                              "decode_step_ms_solo_on_partition": round(t_d, 3), "decode_step_ms_corun": round(t_dc, 3)})
-                log(f"co-run decode {p} / {other} {256 - p}: {other} {t_oc:.2f} ms (solo {t_o:.2f}), "
-                    f"decode step {t_dc:.3f} ms (solo {t_d:.3f})")
+        corun = measure_corun(nova, torch, st, srv)
         result["corun"] = corun
         # offload: the Sec. 3.5 ring against the resident encoder, with the Eq. 8 bandwidth check
         result["offload"] = measure_offload(nova, torch, st, srv)
@@ -504,30 +709,21 @@ def main():
                                    "decode_cus_with_prefill": d} for a, b, c, d in sched.pareto_front(curves, out_len)]
         log(f"Eq. 3 optimum: decode {pv} CUs beside encode, {pp} beside prefill, expected E2E {lat:.3f} s")
         # serving: Poisson bursts through the Alg. 1 policy, co-run partitions vs time slicing
-        serving = []
         result["rate_optimum"] = []
         for rate in args.rates:
             # the Pareto point for this rate: Eq. 1 plus the Eq. 6 queueing delay of encode + prefill
-            rv, rp, rlat = sched.best_under_load(curves, out_len, rate)
+            rv, rp, rlat = sched.best_under_load(sched.on_granule(curves), out_len, rate)
             result["rate_optimum"].append({"rate_req_s": rate, "decode_cus_with_encode": rv,
                                            "decode_cus_with_prefill": rp, "expected_e2e_s": round(rlat, 4)})
-            log(f"rate {rate}: Eq. 1 + Eq. 6 optimum decode {rv} CUs beside encode, {rp} beside prefill, "
-                f"expected E2E {rlat:.3f} s")
-            for mode, kw in [("nova_eq3_static", dict(mode="nova", decode_cus=(pv, pp))),
-                             ("nova_rate_static", dict(mode="nova", decode_cus=(rv, rp))),
-                             ("nova_adaptive", dict(mode="nova", decode_cus=(pv, pp), alpha=32, minimum=32)),
-                             ("time_sliced", dict(mode="time_sliced")),
-                             ("multi_stream", dict(mode="multi_stream"))]:
-                trace = serve.poisson_trace(rate, args.window, seed=3)
-                res = srv.serve(kw, trace)
-                res.update({"mode": mode, "rate_req_s": rate, "window_s": args.window,
-                            "decode_cus": list(kw.get("decode_cus", (256, 256)))})
-                serving.append(res)
-                log(f"serve {mode:16s} rate {rate}: max E2E {res['max_e2e_s']:.3f} s, avg {res['avg_e2e_s']:.3f} s, "
-                    f"avg TBT {res['avg_tbt_ms']:.1f} ms, {res['throughput_req_s']:.2f} req/s, decode batch "
-                    f"{res['avg_decode_batch']:.2f}, vision wait {res['avg_queue_wait_s']:.3f} s (Eq. 6: "
-                    f"{res['eq6_predicted_wait_s']})")
-        result["serving"] = serving
+        sv = run_serving(serve, sched, srv, curves, out_len, args.rates, args.seeds, args.window,
+                         timeline_at=(args.rates[-1], args.seeds[0]))
+        result["adaptive_params"] = {k: v for k, v in sv["adaptive_params"].items() if k != "points"}
+        result["serving"] = sv["summary"]
+        result["serving_runs"] = [{k: v for k, v in r.items() if k not in ("partition_timeline", "arrivals_ms")}
+                                  for r in sv["runs"]]
+        result["partition_timeline"] = next((dict(mode=r["mode"], rate_req_s=r["rate_req_s"], seed=r["seed"],
+                                                  timeline=r["partition_timeline"], arrivals_ms=r["arrivals_ms"])
+                                             for r in sv["runs"] if "partition_timeline" in r), None)
 
     if not args.no_cpu:
         log("timing the oracle on the host (bounded sample)")

@@ -318,6 +318,18 @@ __device__ __forceinline__ void lds_dma16(const bf16_t* g, bf16_t* l_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l_base, 16, 0, 0);
 }
 
+// The same 16-byte LDS-DMA load written as inline assembly, to the LDS byte address lds_addr
+// (wave-uniform, passed in M0).  The compiler does not track it: a fragment read that follows it
+// in program order is not made to wait for it, so the caller orders DMA and reads itself with
+// s_waitcnt and barriers.
+__device__ __forceinline__ void lds_dma16_untracked(const bf16_t* g, uint32_t lds_addr) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"{m0}"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(g)
+               : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
 template <typename OT, int EPI, int BM, int BN, int WM, int WN>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(GemmArgs p) {
   constexpr int TM = WM / 16, TN = WN / 16;
@@ -391,6 +403,79 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   const int off1 = fr * BK + 8 * ((fk + 4) ^ sw);    // sub-step 1
   // K slices are kslice long except the last, which takes what remains
   const int nk = (p.kslice ? min(p.kslice, p.K - (int)k_off) : p.K) / BK;
+  if constexpr (BM == 256 && BN == 256 && WM == 64 && WN == 128) {
+    // 256x256 tiles: each 64-wide K step is two halves of 32 MFMAs per wave.  A wave reads the
+    // fragments of the next half and issues its share of the next stage's DMA in groups spread
+    // between the MFMA rows of the current half, so LDS reads, DMA and MFMAs overlap instead of
+    // running as phases; one wait and barrier per step sits between the two halves.  The DMA is
+    // the untracked form (the compiler would otherwise make each fragment read wait for every
+    // DMA in flight); stage s+1 lands while stage s is multiplied.
+    static_assert(IA == 4 && IB == 4 && TM == 4 && TN == 8, "schedule written for 8 waves of 64x128");
+    const uint32_t lbase = lds_addr_of(lds);
+    uint32_t dst[IA + IB];
+    const bf16_t* src[IA + IB];
+#pragma unroll
+    for (int t = 0; t < IA; ++t) {
+      src[t] = asrc[t];
+      dst[t] = (uint32_t)((wave * IA + t) * 8 * BK) * 2u;
+    }
+#pragma unroll
+    for (int t = 0; t < IB; ++t) {
+      src[IA + t] = bsrc[t];
+      dst[IA + t] = (uint32_t)(BM * BK + (wave * IB + t) * 8 * BK) * 2u;
+    }
+    Frag8 xa[TM], xb[TN], ya[TM], yb[TN];
+    // fragment idx (0..11) of a half: A rows 0..3, then B columns 0..7
+    auto rd = [&](int stage, int off, int idx, Frag8 (&fa)[TM], Frag8 (&fb)[TN]) {
+      const bf16_t* base = lds + stage * STAGE;
+      if (idx < TM) fa[idx] = *reinterpret_cast<const Frag8*>(base + (wm * WM + idx * 16) * BK + off);
+      else fb[idx - TM] = *reinterpret_cast<const Frag8*>(base + BM * BK + (wn * WN + (idx - TM) * 16) * BK + off);
+    };
+    // MFMA row i of (ca, cb) for i = 0..3, each preceded by 3 fragment reads of the next half
+    // (stage rstage, offset roff) and 2 DMA instructions of K step dkt (if dkt >= 0) into dstage
+    auto half = [&](const Frag8 (&ca)[TM], const Frag8 (&cb)[TN], int rstage, int roff, Frag8 (&na)[TM],
+                    Frag8 (&nb)[TN], bool do_read, int dkt, int dstage) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (dkt >= 0) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+            lds_dma16_untracked(src[2 * i + t] + dkt * BK, lbase + (uint32_t)(dstage * STAGE) * 2u + dst[2 * i + t]);
+        }
+        if (do_read) {
+#pragma unroll
+          for (int r = 0; r < 3; ++r) rd(rstage, roff, 3 * i + r, na, nb);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(ca[i], cb[j], acc[i][j]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    // prologue: stages 0 and 1 in flight, wait for stage 0, read the first half of stage 0
+#pragma unroll
+    for (int t = 0; t < IA + IB; ++t) lds_dma16_untracked(src[t], lbase + dst[t]);
+    if (nk > 1) {
+#pragma unroll
+      for (int t = 0; t < IA + IB; ++t) lds_dma16_untracked(src[t] + BK, lbase + (uint32_t)STAGE * 2u + dst[t]);
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (IA + IB));   // vmcnt(8): stage 0 landed, stage 1 may fly
+    } else {
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < 12; ++r) rd(0, off0, r, xa, xb);
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt & 1;
+      half(xa, xb, cur, off1, ya, yb, true, -1, 0);          // first half; read the second half
+      __builtin_amdgcn_s_waitcnt(0);                          // own DMA of stage kt+1 and own reads done
+      __syncthreads();                                        // everyone's: stage kt+1 visible, buffer cur free
+      half(ya, yb, cur ^ 1, off0, xa, xb, kt + 1 < nk, kt + 2 < nk ? kt + 2 : -1, cur);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();                                          // the epilogue reuses the stage buffers
+  } else {
   dma(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -424,6 +509,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  }
   }
 
   if constexpr (EPI == EPI_STORE && sizeof(OT) == 4) {

@@ -112,3 +112,58 @@ def decode_cus(n_pending: int, optimum: int, alpha: int, minimum: int, granule: 
     never below the floor; rounded down to the mask granule."""
     cus = max(minimum, optimum - alpha * (max(n_pending, 1) - 1))
     return max(granule, cus // granule * granule)
+
+
+def on_granule(c: StageCurves, granule: int = GRANULE) -> StageCurves:
+    """The curves at every multiple of `granule` between the smallest and largest measured
+    shares, linear between measured neighbours (masks come in steps of one CU per XCD)."""
+    pts = sorted(c.shares)
+    grid = list(range(pts[0], pts[-1] + 1, granule))
+
+    def lerp(d):
+        out = {}
+        for p in grid:
+            hi = next(q for q in pts if q >= p)
+            lo = max(q for q in pts if q <= p)
+            out[p] = d[lo] if hi == lo else d[lo] + (d[hi] - d[lo]) * (p - lo) / (hi - lo)
+        return out
+    return StageCurves(grid, lerp(c.t_vision), lerp(c.t_prefill), lerp(c.t_dec_vision), lerp(c.t_dec_prefill))
+
+
+def adaptive_params(c: StageCurves, out_len: float, rates, granule: int = GRANULE, tbt_factor: float = 2.0):
+    """Hyperparameters of Eq. 5 from the measured curves (Sec. 3.3.2; the paper picks them per
+    stage pair from its Pareto analysis, Sec. 5.1):
+
+    * SM_op: Eq. 3's optimum for each pair (decode beside encode, decode beside prefill);
+    * for each rate, the Pareto point it calls for (Eq. 1 plus the Eq. 6 wait, best_under_load)
+      gives a decode share, and Little's law gives the requests pending in encode / prefill,
+      N = rate * (E[W_q] + E[T]);
+    * alpha: the least-squares slope of SM_op - share against N - 1 over the rates with N > 1
+      (Eq. 5's linear decrease), rounded to whole CUs, never negative;
+    * SM_min: the smallest share whose co-run decode step stays within tbt_factor times the step
+      at SM_op (the floor bounds TBT).
+    All on the granule-interpolated curves.  Returns a dict, with the per-rate points."""
+    g = on_granule(c, granule)
+    op_v, op_p, _ = best_static(g, out_len)
+    pts = []
+    for r in rates:
+        pv, pp, lat = best_under_load(g, out_len, r)
+        t = g.t_vision[pv] + g.t_prefill[pp]
+        w = queue_wait(t, r)
+        if w == float("inf"):
+            continue
+        pts.append({"rate": r, "decode_cus_with_encode": pv, "decode_cus_with_prefill": pp,
+                    "pending": r * (w + t), "expected_e2e_s": lat})
+
+    def slope(op, key):
+        num = sum((op - q[key]) * (q["pending"] - 1) for q in pts if q["pending"] > 1)
+        den = sum((q["pending"] - 1) ** 2 for q in pts if q["pending"] > 1)
+        return max(0, int(round(num / den))) if den > 0 else 0
+
+    def floor(op, dec):
+        lim = tbt_factor * dec[op]
+        return min(p for p in g.shares if dec[p] <= lim)
+    return {"sm_op_v": op_v, "sm_op_p": op_p,
+            "alpha_v": slope(op_v, "decode_cus_with_encode"), "alpha_p": slope(op_p, "decode_cus_with_prefill"),
+            "sm_min": max(floor(op_v, g.t_dec_vision), floor(op_p, g.t_dec_prefill), granule),
+            "granule": granule, "tbt_factor": tbt_factor, "points": pts}

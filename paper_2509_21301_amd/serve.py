@@ -87,7 +87,8 @@ class Server:
     def __init__(self, vit, llm, kv, pixels, mode="nova", decode_cus=(96, 96), alpha=0, minimum=32, max_batch=32,
                  max_blocks=256, device="cuda", slice_order="alternate", decode_limit=None):
         """decode_cus = (P_v, P_p): decode's CUs while co-running with vision encode / prefill
-        (Eq. 3's optimum); alpha > 0 turns on the Eq. 5 adaptation with floor `minimum`.
+        (Eq. 3's optimum); alpha > 0 (one value, or one per pair as (alpha_v, alpha_p)) turns on
+        the Eq. 5 adaptation with floor `minimum`.
         slice_order / decode_limit choose the time-sliced driver's pass order (see
         _slice_decode_next)."""
         if slice_order not in ("alternate", "decode_first", "prefill_first"):
@@ -112,6 +113,7 @@ class Server:
         self.partition_log = []
         self.decode_batches = []      # batch size of every decode step
         self.sched_us = []            # scheduler time per handled event (host, microseconds)
+        self.worker_us = []           # worker time per pass to pick and switch its partition (host, us)
 
     # ---------------------------------------------------------------- partitions
     def _masks(self, stage):
@@ -125,16 +127,23 @@ class Server:
         if stage != nova.STAGE_DECODE and dec == 0:
             return FULL
         pair = stage if stage != nova.STAGE_DECODE else other
-        op = self.decode_cus[0] if pair == nova.STAGE_ENCODE else self.decode_cus[1]
-        p = sched.decode_cus(pend, op, self.alpha, self.minimum) if self.alpha else op
+        i = 0 if pair == nova.STAGE_ENCODE else 1
+        op = self.decode_cus[i]
+        alpha = self.alpha[i] if isinstance(self.alpha, (tuple, list)) else self.alpha
+        p = sched.decode_cus(pend, op, alpha, self.minimum) if alpha else op
         return nova.make_cu_mask(p, 0) if stage == nova.STAGE_DECODE else nova.make_cu_mask(256 - p, p // 8)
 
     def _stream(self, stage):
+        """The stream for the next forward pass of `stage` (the worker-side partition step, once
+        per pass; its host time is the worker overhead of Sec. 5.7)."""
         if self.mode == "time_sliced":
             return torch.cuda.current_stream()
+        t0 = time.perf_counter()
         mask = self._masks(stage)
         s = nova.set_stage_partition(stage, mask)
-        self.partition_log.append((time.perf_counter(), stage, sum(bin(w).count("1") for w in mask)))
+        t1 = time.perf_counter()
+        self.worker_us.append((t1 - t0) * 1e6)
+        self.partition_log.append((t1, stage, sum(bin(w).count("1") for w in mask)))
         return s
 
     # ---------------------------------------------------------------- stage passes
@@ -390,10 +399,11 @@ class Server:
         bs = np.array(self.decode_batches or [0])
         out["decode_steps"] = int(len(self.decode_batches))
         out["avg_decode_batch"] = round(float(bs.mean()), 3)
-        if self.sched_us:
-            us = np.array(self.sched_us)
-            out["sched_event_us"] = {"p50": round(float(np.percentile(us, 50)), 1), "p99": round(float(np.percentile(us, 99)), 1),
-                                     "max": round(float(us.max()), 1), "events": int(len(us))}
+        for key, vals in (("sched_event_us", self.sched_us), ("worker_partition_us", self.worker_us)):
+            if vals:
+                us = np.array(vals)
+                out[key] = {f"p{q}": round(float(np.percentile(us, q)), 1) for q in (10, 50, 90, 99)}
+                out[key].update(max=round(float(us.max()), 1), n=int(len(us)))
         return out
 
 
@@ -414,4 +424,5 @@ def summarize(trace, rate=None):
             "avg_tbt_ms": round(float(tbt.mean()) * 1e3, 3), "max_tbt_ms": round(float(tbt.max()) * 1e3, 3),
             "avg_queue_wait_s": round(float(qwait.mean()), 4), "throughput_req_s": round(len(trace) / span, 3),
             "mean_service_s": round(float(service.mean()), 4),
+            "mean_service2_s2": round(float((service ** 2).mean()), 6),
             "eq6_predicted_wait_s": None if pred == float("inf") else round(pred, 4)}

@@ -84,3 +84,41 @@ def test_mg1_wait_matches_oracle():
     assert sched.mg1_wait(4.0, 0.25, 0.1) == float("inf")
     # deterministic service reduces to the fixed-T form used by the rate-aware search
     assert abs(sched.mg1_wait(3.0, 0.2, 0.04) - sched.queue_wait(0.2, 3.0)) < 1e-12
+
+
+def test_curves_on_the_8_cu_granule():
+    c = curves(4)
+    g = sched.on_granule(c)
+    assert g.shares == list(range(32, 225, 8))
+    for p in SHARES:                                          # measured points kept exactly
+        assert g.t_vision[p] == c.t_vision[p] and g.t_dec_prefill[p] == c.t_dec_prefill[p]
+    assert abs(g.t_vision[40] - (0.75 * c.t_vision[32] + 0.25 * c.t_vision[64])) < 1e-15
+    assert abs(g.t_dec_vision[112] - 0.5 * (c.t_dec_vision[96] + c.t_dec_vision[128])) < 1e-15
+
+
+def test_adaptive_params_from_the_pareto_points():
+    """Eq. 5's SM_op, alpha and SM_min derived from the curves: SM_op is Eq. 3's optimum on the
+    granule curves, the rate-aware decode shares never grow with the rate, alpha is the
+    least-squares slope of their decrease against the pending count, and the floor keeps the
+    decode step within the TBT bound."""
+    c = curves(7)
+    rates = [0.5, 1, 2, 4, 6, 8, 10]
+    a = sched.adaptive_params(c, 32, rates)
+    g = sched.on_granule(c)
+    pv, pp, _ = sched.best_static(g, 32)
+    assert (a["sm_op_v"], a["sm_op_p"]) == (pv, pp)
+    pts = a["points"]
+    assert len(pts) >= 3 and all(q["pending"] > 0 for q in pts)
+    shares = [q["decode_cus_with_encode"] + q["decode_cus_with_prefill"] for q in pts]
+    assert shares == sorted(shares, reverse=True)
+    for key, op, alpha in (("decode_cus_with_encode", pv, a["alpha_v"]), ("decode_cus_with_prefill", pp, a["alpha_p"])):
+        xs = np.array([q["pending"] - 1 for q in pts if q["pending"] > 1])
+        ys = np.array([op - q[key] for q in pts if q["pending"] > 1])
+        want = max(0, int(round((xs * ys).sum() / (xs * xs).sum()))) if len(xs) else 0
+        assert alpha == want
+    assert 8 <= a["sm_min"] <= min(pv, pp)
+    assert g.t_dec_vision[a["sm_min"]] <= 2.0 * g.t_dec_vision[pv] or g.t_dec_prefill[a["sm_min"]] <= 2.0 * g.t_dec_prefill[pp]
+    # Little's law for one point by hand
+    q = pts[0]
+    t = g.t_vision[q["decode_cus_with_encode"]] + g.t_prefill[q["decode_cus_with_prefill"]]
+    assert abs(q["pending"] - q["rate"] * (osched.mg1_wait(q["rate"], t, t * t) + t)) < 1e-9

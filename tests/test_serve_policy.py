@@ -102,7 +102,8 @@ def test_alg1_policy(mode):
     assert abs(res["avg_decode_batch"] - sum(len(b) for b in batches) / len(batches)) < 1e-3
     assert res["mean_service_s"] > 0 and "eq6_predicted_wait_s" in res
     if mode == "nova":
-        assert res["sched_event_us"]["events"] >= 2 * len(trace)
+        assert res["sched_event_us"]["n"] >= 2 * len(trace)
+        assert res["sched_event_us"]["p10"] <= res["sched_event_us"]["p50"] <= res["sched_event_us"]["p99"]
 
 
 def test_decode_positions_after_prefill():
