@@ -196,7 +196,7 @@ class ServingSetup:
     n_slots > 0 the encoder's layers stay in pinned host memory and stream through that many
     device slots (Sec. 3.5); kv_blocks sizes the paged KV pool."""
 
-    def __init__(self, nova, torch, synth, st, n_slots=0, kv_blocks=12000):
+    def __init__(self, nova, torch, synth, st, n_slots=0, kv_blocks=30000):
         self.nova, self.torch, self.synth, self.st = nova, torch, synth, st
         cfg = synth.VIT_SCREEN
         gen = torch.Generator(device="cuda")
@@ -339,6 +339,92 @@ def measure_corun(nova, torch, st, srv):
     return corun
 
 
+# ----------------------------------------------------------------------------- linear co-run study
+def linear_corun(nova, torch, synth, n_dec=2000, n_vis=200):
+    """The two-linear experiment of Sec. 3.2.1 (its linear co-run table and the SM sweep) and the
+    intra-CU variant of Sec. 3.2.3 on MI355X: the vision MLP up-projection at the screenshot shape
+    (13416 x 1280 -> 5120) repeated n_vis times and the decode gate/up projection at batch 3
+    (3 x 3584 -> 2 x 18944) repeated n_dec times, each alone, both at once on unrestricted streams,
+    on complementary CU partitions, and as the low-footprint pair (128x128-tile GEMM + vector-ALU
+    decode linear without LDS) sharing every CU.  Per-launch times come from HIP events on each
+    stream; the makespan spans the first and last event of both."""
+    full = [0xFFFFFFFF] * 8
+    g = torch.Generator(device="cuda")
+    g.manual_seed(17)
+    xv = (torch.randn(13416, 1280, generator=g, device="cuda")).to(torch.bfloat16)
+    wv = (torch.randn(5120, 1280, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    ov = torch.zeros(13416, 5120, dtype=torch.float32, device="cuda")
+    xd = (torch.randn(3, 3584, generator=g, device="cuda")).to(torch.bfloat16)
+    wd = (torch.randn(2 * 18944, 3584, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    od = torch.zeros(3, 2 * 18944, dtype=torch.float32, device="cuda")
+
+    def run(vis_variant, dec_variant, vis_cus, dec_cus, nv, nd):
+        sv = nova.set_stage_partition(nova.STAGE_ENCODE, full if vis_cus == 256 else nova.make_cu_mask(vis_cus, 256 // 8 - vis_cus // 8))
+        sd = nova.set_stage_partition(nova.STAGE_DECODE, full if dec_cus == 256 else nova.make_cu_mask(dec_cus, 0))
+        torch.cuda.synchronize()
+        ev_v = [torch.cuda.Event(enable_timing=True) for _ in range(nv + 1)]
+        ev_d = [torch.cuda.Event(enable_timing=True) for _ in range(nd + 1)]
+        if nv:
+            ev_v[0].record(sv)
+        if nd:
+            ev_d[0].record(sd)
+        iv = idd = 0
+        while iv < nv or idd < nd:          # enqueue both streams in proportion
+            if idd < nd and (iv >= nv or idd * nv <= iv * nd):
+                nova.linear(dec_variant, xd, wd, od, stream=sd)
+                idd += 1
+                ev_d[idd].record(sd)
+            else:
+                nova.linear(vis_variant, xv, wv, ov, stream=sv)
+                iv += 1
+                ev_v[iv].record(sv)
+        torch.cuda.synchronize()
+        out = {"vision_cus": vis_cus, "decode_cus": dec_cus}
+        starts, ends = [], []
+        for name, ev, n, flops in (("vision", ev_v, nv, 2.0 * 13416 * 1280 * 5120), ("decode", ev_d, nd, None)):
+            if not n:
+                continue
+            t = np.array([a.elapsed_time(b) for a, b in zip(ev, ev[1:])])
+            out[name] = {"launches": n, "total_ms": round(float(t.sum()), 2), "mean_us": round(float(t.mean()) * 1e3, 1),
+                         "p50_us": round(float(np.percentile(t, 50)) * 1e3, 1),
+                         "p99_us": round(float(np.percentile(t, 99)) * 1e3, 1),
+                         "cv": round(float(t.std() / t.mean()), 3)}
+            if flops:
+                out[name]["tflops"] = round(flops / (t.mean() / 1e3) / 1e12, 1)
+            else:
+                out[name]["hbm_gbs"] = round(wd.numel() * 2 / (t.mean() / 1e3) / 1e9, 1)
+            starts.append(ev[0])
+            ends.append(ev[-1])
+        out["makespan_ms"] = round(max(starts[0].elapsed_time(e) for e in ends), 2) if starts else 0.0
+        return out
+
+    res = {"workload": "vision fc1 13416x1280->5120 (x%d), decode gate/up 3x3584->37888 (x%d)" % (n_vis, n_dec)}
+    for v in (nova.LINEAR_TILED, nova.LINEAR_TILED_SMALL):      # warm every kernel once
+        nova.linear(v, xv, wv, ov)
+    for v in (nova.LINEAR_THIN, nova.LINEAR_THIN_VALU):
+        nova.linear(v, xd, wd, od)
+    torch.cuda.synchronize()
+    T, TS, D, DV = nova.LINEAR_TILED, nova.LINEAR_TILED_SMALL, nova.LINEAR_THIN, nova.LINEAR_THIN_VALU
+    res["solo_vision"] = run(T, D, 256, 256, n_vis, 0)
+    res["solo_decode"] = run(T, D, 256, 256, 0, n_dec)
+    res["sequential_ms"] = round(res["solo_vision"]["makespan_ms"] + res["solo_decode"]["makespan_ms"], 2)
+    res["corun_unpartitioned"] = run(T, D, 256, 256, n_vis, n_dec)
+    res["corun_partitioned"] = [run(T, D, 256 - p, p, n_vis, n_dec) for p in (16, 32, 48, 64, 96, 128)]
+    res["solo_vision_small_tiles"] = run(TS, DV, 256, 256, n_vis, 0)
+    res["solo_decode_valu"] = run(TS, DV, 256, 256, 0, n_dec)
+    res["sequential_low_footprint_ms"] = round(res["solo_vision_small_tiles"]["makespan_ms"] +
+                                               res["solo_decode_valu"]["makespan_ms"], 2)
+    res["corun_intra_cu"] = run(TS, DV, 256, 256, n_vis, n_dec)
+    for key in ("corun_unpartitioned", "corun_intra_cu"):
+        r = res[key]
+        log(f"linear co-run {key}: makespan {r['makespan_ms']} ms (sequential {res['sequential_ms']} ms); vision "
+            f"{r['vision']['mean_us']} us cv {r['vision']['cv']}, decode {r['decode']['mean_us']} us cv {r['decode']['cv']}")
+    for r in res["corun_partitioned"]:
+        log(f"linear co-run decode on {r['decode_cus']} CUs: makespan {r['makespan_ms']} ms; vision {r['vision']['mean_us']} us, "
+            f"decode {r['decode']['mean_us']} us")
+    return res
+
+
 # ----------------------------------------------------------------------------- offload (Sec. 3.5)
 def measure_offload(nova, torch, st, srv, slots=(2, 3, 4, 5)):
     """The encoder with its 32 layers in pinned host memory, streamed through K device slots (Eq. 7),
@@ -356,9 +442,9 @@ def measure_offload(nova, torch, st, srv, slots=(2, 3, 4, 5)):
     work = [("screenshot_1092x2408_b1", srv.vit, srv.pixels, srv.vis),
             ("image_1008x1008_b1", st.vit, st.pixels[:1], st.enc_out[:1]),
             ("image_1008x1008_b8", st.vit, st.pixels, st.enc_out)]
-    def per_pass(fn, warm=2, reps=5):
-        # back-to-back passes (so a pass's head copies overlap the previous pass's tail), one event between
-        # each two; median and best, since a pass now and then runs long on this machine, resident ones too
+    def pass_times(fn, warm, reps):
+        # back-to-back passes (so a pass's head copies overlap the previous pass's tail), one event
+        # between each two
         for _ in range(warm):
             fn()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
@@ -367,7 +453,11 @@ def measure_offload(nova, torch, st, srv, slots=(2, 3, 4, 5)):
             fn()
             ev[i + 1].record(stream)
         ev[-1].synchronize()
-        ts = sorted(a.elapsed_time(b) for a, b in zip(ev, ev[1:]))
+        return [a.elapsed_time(b) for a, b in zip(ev, ev[1:])]
+
+    def per_pass(fn, warm=2, reps=5):
+        # median and best, since a pass now and then runs long on this machine, resident ones too
+        ts = sorted(pass_times(fn, warm, reps))
         return ts[len(ts) // 2], ts[0]
 
     rows = []
@@ -379,6 +469,9 @@ def measure_offload(nova, torch, st, srv, slots=(2, 3, 4, 5)):
                "resident_layer_mb": round(L * lb / 1e6, 1)}
         for K in slots:
             ov = nova.Vit(vit.cfg, None, blobs=(vit.embed, host, vit.head, lb), n_slots=K)
+            if K == slots[0]:
+                # the first passes of a freshly built ring, one by one (the warm-up anomaly)
+                row["fresh_ring_passes_ms"] = [round(t, 3) for t in pass_times(lambda: ov.encode(px, out=out), 0, 8)]
             t_off, t_off_min = per_pass(lambda: ov.encode(px, out=out))
             same = bool(torch.equal(out, ref))
             need = (L * lb) / (t_res / 1e3) * (L - K) / (L - 2) / 1e9
@@ -520,6 +613,8 @@ def main():
                     help="only the serving runs under an HBM budget: encoder layers offloaded (K = 2 slots), "
                          "KV pool capped at 40 GB, batch-32 decode (prints their JSON)")
     ap.add_argument("--modes", nargs="+", default=None, help="restrict the serving modes")
+    ap.add_argument("--linear-corun", action="store_true",
+                    help="only the two-linear co-run study (inter-CU partitions vs intra-CU sharing; prints its JSON)")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
     ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32", "copy", "offload"],
                     help="run only this stage in a loop of --steps passes (for rocprofv3); 'copy' is a plain "
@@ -543,6 +638,9 @@ def main():
         log(f"copy 1 GiB: {ms:.3f} ms per pass, {2 * (1 << 30) / (ms / 1e3) / 1e9:.1f} GB/s (read + write)")
         return
     nova.init(0)
+    if args.linear_corun:
+        print(json.dumps({"linear_corun": linear_corun(nova, torch, synth)}), flush=True)
+        return
     st = Stages(nova, torch, synth, device, args.batch)
     vc, lc = st.vc, st.lc
     B = args.batch

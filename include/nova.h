@@ -216,6 +216,22 @@ int nova_llm_decode_noalloc(const nova_llm* llm, const int32_t* ids, const int32
                             int max_blocks, int batch, int max_ctx, const nova_kv* kv, int32_t* next_ids,
                             float* logits, nova_stream_t stream);
 
+/* ------------------------------------------------------------------ linear co-run study
+ * The two-linear experiment behind the paper's choice of inter-CU partitioning (Sec. 3.2.1, its
+ * linear co-run table, and Sec. 3.2.3): one linear layer out[M, N] += x[M, K] w[N, K]^T
+ * (x, w device bf16 row-major, out device fp32, all 256-byte aligned), enqueued on `stream`,
+ * with one of the kernels the stage calls use or the low-footprint pair of the intra-CU variant:
+ *  NOVA_LINEAR_TILED       the encode / prefill GEMM (256x256 or 128x128 tiles as for the stages;
+ *                          K % 64 == 0, N % 128 == 0)
+ *  NOVA_LINEAR_TILED_SMALL the same GEMM held to 128x128 tiles of 4 waves (64 KB of LDS), so a
+ *                          CU keeps room for another kernel's workgroups
+ *  NOVA_LINEAR_THIN        the decode thin GEMM on the matrix cores (M <= 32, K % 256 == 0,
+ *                          N % 64 == 0, and N large enough that K is not split on the stream's CUs)
+ *  NOVA_LINEAR_THIN_VALU   the decode linear on the vector ALUs without LDS (M <= 4, K % 512 == 0)
+ * Returns NOVA_EUNSUPPORTED outside those shapes. */
+enum { NOVA_LINEAR_TILED = 0, NOVA_LINEAR_TILED_SMALL = 1, NOVA_LINEAR_THIN = 2, NOVA_LINEAR_THIN_VALU = 3 };
+int nova_linear(int variant, const void* x, int M, int K, const void* w, int N, float* out, nova_stream_t stream);
+
 /* ------------------------------------------------------------------ CU partitions (Sec. 3.2.2)
  * gfx950 deals a kernel's workgroups round-robin over its 8 XCDs, and a CU-mask bit i selects
  * CU slot i/32 of shader engine (i/8)%4 of XCD i%8.  A partition therefore never confines a

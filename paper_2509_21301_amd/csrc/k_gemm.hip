@@ -404,13 +404,16 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   // K slices are kslice long except the last, which takes what remains
   const int nk = (p.kslice ? min(p.kslice, p.K - (int)k_off) : p.K) / BK;
   if constexpr (BM == 256 && BN == 256 && WM == 64 && WN == 128) {
-    // 256x256 tiles: each 64-wide K step is two halves of 32 MFMAs per wave.  A wave reads the
-    // fragments of the next half and issues its share of the next stage's DMA in groups spread
-    // between the MFMA rows of the current half, so LDS reads, DMA and MFMAs overlap instead of
-    // running as phases; one wait and barrier per step sits between the two halves.  The DMA is
-    // the untracked form (the compiler would otherwise make each fragment read wait for every
-    // DMA in flight); stage s+1 lands while stage s is multiplied.
-    static_assert(IA == 4 && IB == 4 && TM == 4 && TN == 8, "schedule written for 8 waves of 64x128");
+    // 256x256 tiles (the same schedule measured slower for the 4-wave 128x128 tiles, whose
+    // halves have too few MFMAs to cover the reads).  Each 64-wide K step is two halves of TM x TN
+    // MFMAs per wave.  A wave reads the fragments
+    // of the next half and issues its share of the next stage's DMA in groups spread between the
+    // MFMA rows of the current half, so LDS reads, DMA and MFMAs overlap instead of running as
+    // phases; one wait and barrier per step sits between the two halves.  The DMA is the
+    // untracked form (the compiler would otherwise make each fragment read wait for every DMA in
+    // flight); stage s+1 lands while stage s is multiplied.
+    constexpr int NF = TM + TN, RPG = NF / TM;     // fragments per half, fragment reads per MFMA row
+    static_assert(RPG * TM == NF, "fragment reads must split evenly over the MFMA rows");
     const uint32_t lbase = lds_addr_of(lds);
     uint32_t dst[IA + IB];
     const bf16_t* src[IA + IB];
@@ -425,13 +428,13 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
       dst[IA + t] = (uint32_t)(BM * BK + (wave * IB + t) * 8 * BK) * 2u;
     }
     Frag8 xa[TM], xb[TN], ya[TM], yb[TN];
-    // fragment idx (0..11) of a half: A rows 0..3, then B columns 0..7
+    // fragment idx (0..NF-1) of a half: A rows 0..TM-1, then B columns 0..TN-1
     auto rd = [&](int stage, int off, int idx, Frag8 (&fa)[TM], Frag8 (&fb)[TN]) {
       const bf16_t* base = lds + stage * STAGE;
       if (idx < TM) fa[idx] = *reinterpret_cast<const Frag8*>(base + (wm * WM + idx * 16) * BK + off);
       else fb[idx - TM] = *reinterpret_cast<const Frag8*>(base + BM * BK + (wn * WN + (idx - TM) * 16) * BK + off);
     };
-    // MFMA row i of (ca, cb) for i = 0..3, each preceded by 3 fragment reads of the next half
+    // MFMA row i of (ca, cb) for i = 0..TM-1, each preceded by RPG fragment reads of the next half
     // (stage rstage, offset roff) and 2 DMA instructions of K step dkt (if dkt >= 0) into dstage
     auto half = [&](const Frag8 (&ca)[TM], const Frag8 (&cb)[TN], int rstage, int roff, Frag8 (&na)[TM],
                     Frag8 (&nb)[TN], bool do_read, int dkt, int dstage) {
@@ -445,7 +448,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
         }
         if (do_read) {
 #pragma unroll
-          for (int r = 0; r < 3; ++r) rd(rstage, roff, 3 * i + r, na, nb);
+          for (int r = 0; r < RPG; ++r) rd(rstage, roff, RPG * i + r, na, nb);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -465,7 +468,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < 12; ++r) rd(0, off0, r, xa, xb);
+    for (int r = 0; r < NF; ++r) rd(0, off0, r, xa, xb);
     for (int kt = 0; kt < nk; ++kt) {
       const int cur = kt & 1;
       half(xa, xb, cur, off1, ya, yb, true, -1, 0);          // first half; read the second half
@@ -620,6 +623,9 @@ static void* out_at(const GemmArgs& p, size_t rows, size_t cols) {
 
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
+  if constexpr (sizeof(TA) == 2) {
+    if (p.small_tiles) return launch_dma<OT, EPI, 128, 128, 64, 64>(p, s);
+  }
   // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when there are at least two tiles per
   // CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU), with K split into slices
   // when those tiles cannot fill the GPU (and the caller gave a workspace).  A projection that
@@ -658,6 +664,10 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         return hipGetLastError();
       }
     }
+    // 256x256 tiles that fill at least three quarters of one round of the GPU (one workgroup per
+    // CU) beat two rounds of 128x128 tiles (the 3.6k-token prefill's QKV projection: 14 x 18
+    // tiles, 157 -> 99 us; the one-image encode's QKV and MLP up projections)
+    if (p.N % 256 == 0 && tiles256 >= 192 && tiles256 < 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     if (!(p.N % 256 == 0 && tiles256 >= 512) && p.vt == nullptr) {
       const int sl = split_slices(p);
       if (sl > 1) {
@@ -715,6 +725,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
       }
       return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     }
+    if (p.N % 256 == 0 && tiles >= 192) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     return launch_dma<OT, EPI, 128, 128, 64, 64>(p, s);
   }
   return launch_tile<TA, OT, EPI, 128, 128, 64, 64>(p, s);

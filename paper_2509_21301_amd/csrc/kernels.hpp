@@ -34,6 +34,9 @@ struct GemmArgs {
   // lands at vt[((b * heads + h) * vt_hd + d) * vt_pad + t].  Requires v_col0 % 256 == 0,
   // vt_tokens % 8 == 0 and vt_pad % 8 == 0 (checked by the caller).
   void* vt = nullptr; int v_col0 = 0, vt_hd = 0, vt_tokens = 0, vt_pad = 0;
+  // bf16 only: always 128x128 tiles of 4 waves, unsplit (a kernel that leaves room on every CU for
+  // another kernel's workgroups: the intra-CU co-residency variant)
+  bool small_tiles = false;
 };
 template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s);
@@ -107,6 +110,11 @@ struct DecAttnArgs {
 size_t dec_attn_partial_floats(int B, int n_q, int D, int max_ctx, int n_kv);
 template <typename T>
 hipError_t decode_attention(const DecAttnArgs& p, int head_dim, hipStream_t s);
+
+// Decode linear on the vector ALUs (no LDS, no matrix cores): out[B, ldo] += X[B, K] W[N, K]^T in
+// fp32, B <= 4, K % 512 == 0.  The low-footprint decode kernel of the intra-CU co-residency variant.
+hipError_t gemv_valu(const bf16_t* X, int ldx, const bf16_t* W, int ldw, int B, int N, int K, float* out, int ldo,
+                     hipStream_t s);
 
 // ---- small memory-bound kernels
 // LayerNorm (ln=1, with shift b) or RMSNorm (ln=0) of fp32 rows into T rows.

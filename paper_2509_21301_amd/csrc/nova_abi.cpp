@@ -929,6 +929,42 @@ extern "C" int nova_llm_decode_noalloc(const nova_llm* m, const int32_t* ids, co
   return decode_dispatch(m, ids, pos, tables, max_blocks, batch, max_ctx, kv, next_ids, logits, ws, (hipStream_t)stream);
 }
 
+// ------------------------------------------------------------------ linear co-run study
+extern "C" int nova_linear(int variant, const void* x, int M, int K, const void* w, int N, float* out,
+                           nova_stream_t stream) {
+  if (!x || !w || !out || !aligned(x) || !aligned(w) || !aligned(out))
+    return fail(NOVA_EINVAL, "x, w and out must be non-null and 256-byte aligned");
+  if (M <= 0 || N <= 0 || K <= 0) return fail(NOVA_EINVAL, "non-positive size");
+  hipStream_t s = (hipStream_t)stream;
+  const bf16_t* xb = (const bf16_t*)x;
+  const bf16_t* wb = (const bf16_t*)w;
+  switch (variant) {
+    case NOVA_LINEAR_TILED:
+    case NOVA_LINEAR_TILED_SMALL: {
+      if (K % 64 || N % 128) return fail(NOVA_EUNSUPPORTED, "tiled linear needs K %% 64 == 0 and N %% 128 == 0");
+      GemmArgs p{xb, K, wb, K, M, N, K, nullptr, out, N, nullptr, 0};
+      p.small_tiles = variant == NOVA_LINEAR_TILED_SMALL;
+      CALL(NOVA_KIND_GEMM, s, (nova::gemm<bf16_t, bf16_t>(p, nova::EPI_RESID, s)));
+      return NOVA_OK;
+    }
+    case NOVA_LINEAR_THIN: {
+      const int cus = stream_cus(s);
+      if (M > 32 || K % 256 || N % 64) return fail(NOVA_EUNSUPPORTED, "thin linear needs M <= 32, K %% 256 == 0, N %% 64 == 0");
+      if (nova::gemv_splits(N, K, M, false, cus) != 1)
+        return fail(NOVA_EUNSUPPORTED, "thin linear of %d rows would split K on %d CUs (no workspace here)", N, cus);
+      GemvArgs p{xb, K, wb, K, M, N, K, out, N, nullptr, nullptr};
+      p.cus = cus;
+      CALL(NOVA_KIND_GEMV, s, (nova::gemv<bf16_t, float>(p, nova::EPI_RESID, s)));
+      return NOVA_OK;
+    }
+    case NOVA_LINEAR_THIN_VALU:
+      if (M > 4 || K % 512) return fail(NOVA_EUNSUPPORTED, "vector-ALU linear needs M <= 4 and K %% 512 == 0");
+      CALL(NOVA_KIND_GEMV, s, nova::gemv_valu(xb, K, wb, K, M, N, K, out, N, s));
+      return NOVA_OK;
+  }
+  return fail(NOVA_EINVAL, "unknown linear variant %d", variant);
+}
+
 // ------------------------------------------------------------------ CU partitions
 extern "C" int nova_make_cu_mask(int n_cus, int first_slot, uint32_t* mask) {
   if (!mask) return fail(NOVA_EINVAL, "null mask");

@@ -82,6 +82,7 @@ _SIG = {
                                   C.POINTER(KvC), C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "nova_llm_decode_noalloc": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_int,
                                           C.POINTER(KvC), C.c_void_p, C.c_void_p, C.c_void_p]),
+    "nova_linear": (C.c_int, [C.c_int, C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p]),
     "nova_make_cu_mask": (C.c_int, [C.c_int, C.c_int, C.POINTER(C.c_uint32)]),
     "nova_set_stage_partition": (C.c_int, [C.c_int, C.POINTER(C.c_uint32), C.c_int, C.POINTER(C.c_void_p)]),
     "nova_cu_probe": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int]),
@@ -405,6 +406,18 @@ class Llm:
         if h is not None and h.value and lib is not None:
             lib.nova_llm_destroy(h)
             self.h = None
+
+
+# ----------------------------------------------------------------------------- linear co-run study
+LINEAR_TILED, LINEAR_TILED_SMALL, LINEAR_THIN, LINEAR_THIN_VALU = 0, 1, 2, 3
+
+
+def linear(variant: int, x, w, out, stream=None):
+    """out (fp32 [M, N]) += x (bf16 [M, K]) w (bf16 [N, K])^T with the chosen kernel variant."""
+    m, k = x.shape
+    n = w.shape[0]
+    _check(lib.nova_linear(variant, _ptr(x), m, k, _ptr(w), n, _ptr(out), _stream(stream)))
+    return out
 
 
 # ----------------------------------------------------------------------------- partitions & timing

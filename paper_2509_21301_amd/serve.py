@@ -78,6 +78,17 @@ class BlockPool:
                 raise nova.NovaError(nova.ENOKV, f"KV pool exhausted ({n} blocks wanted, {len(self.free)} free)")
             return [self.free.pop() for _ in range(n)]
 
+    def try_take(self, n):
+        """n blocks, or None (nothing taken) when fewer are free."""
+        with self.lock:
+            if len(self.free) < n:
+                return None
+            return [self.free.pop() for _ in range(n)]
+
+    def available(self):
+        with self.lock:
+            return len(self.free)
+
     def give(self, blocks):
         with self.lock:
             self.free.extend(blocks)
@@ -192,20 +203,36 @@ class Server:
             r.t_tokens.append(now)
 
     # ---------------------------------------------------------------- admission
-    def _admit(self, req, ids_seed):
-        need = (self.n_vis + req.n_text + req.n_out + self.cfg.block - 1) // self.cfg.block
+    def _blocks_needed(self, req):
+        return (self.n_vis + req.n_text + req.n_out + self.cfg.block - 1) // self.cfg.block
+
+    def _prepare(self, req, ids_seed):
+        need = self._blocks_needed(req)
         if need > self.max_blocks:
             raise nova.NovaError(nova.EINVAL, "request longer than the block table")
-        req.blocks = self.blocks.take(need)
-        row = np.full(self.max_blocks, -1, np.int32)
-        row[:need] = req.blocks
-        req.table_row = row
+        if need > self.kv.num_blocks:
+            raise nova.NovaError(nova.ENOKV, "request longer than the whole KV pool")
         req.ids = torch.from_numpy(synth.text_ids(req.n_text, self.cfg.vocab, seed=ids_seed)).to(self.device)
+
+    def _reserve(self, req):
+        """KV blocks for the whole request, taken when it is about to start vision encode; False
+        (the request keeps waiting) while the pool has too few free blocks."""
+        if req.blocks:
+            return True
+        need = self._blocks_needed(req)
+        blocks = self.blocks.try_take(need)
+        if blocks is None:
+            return False
+        req.blocks = blocks
+        row = np.full(self.max_blocks, -1, np.int32)
+        row[:need] = blocks
+        req.table_row = row
+        return True
 
     # ---------------------------------------------------------------- run
     def run(self, trace, seed=0):
         for r in trace:
-            self._admit(r, seed * 100003 + r.rid)
+            self._prepare(r, seed * 100003 + r.rid)
         if self.device == "cuda":
             torch.cuda.synchronize()
         if self.mode == "time_sliced":
@@ -274,7 +301,7 @@ class Server:
         finished = 0
 
         def try_vision():
-            if q_vision and not busy["vision"] and not busy["prefill"]:
+            if q_vision and not busy["vision"] and not busy["prefill"] and self._reserve(q_vision[0]):
                 r = q_vision.pop(0)
                 busy["vision"] = True
                 with self.lock:
@@ -326,6 +353,7 @@ class Server:
                     self.decode_active -= 1
                 self.blocks.give(r.blocks)
                 finished += 1
+                try_vision()                      # freed KV blocks may admit the next request
             self.sched_us.append((time.perf_counter() - t_ev) * 1e6)
         stop.set()
         vq.put(None)
@@ -364,7 +392,8 @@ class Server:
                 q_vision.append(r)
             while q_decode and len(batch) < self.max_batch:   # join at a step boundary
                 batch.append(q_decode.pop(0))
-            if self._slice_decode_next(len(batch), len(batch) + len(q_decode), bool(q_prefill or q_vision),
+            vision_ready = bool(q_vision) and self.blocks.available() >= self._blocks_needed(q_vision[0])
+            if self._slice_decode_next(len(batch), len(batch) + len(q_decode), bool(q_prefill) or vision_ready,
                                        last_was_decode):
                 self.decode_batches.append(len(batch))
                 self._decode_step(batch)
@@ -385,7 +414,7 @@ class Server:
                 else:
                     q_decode.append(r)
                 continue
-            if q_vision:
+            if q_vision and self._reserve(q_vision[0]):
                 r = q_vision.pop(0)
                 self._vision(r)
                 q_prefill.append(r)

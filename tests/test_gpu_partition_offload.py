@@ -147,3 +147,64 @@ def test_offload_bit_identical_to_resident(gpu_lib, vit5, k_slots):
         assert copies == k_slots + (call + 1) * VIT5.layers
         assert slots == osched.ring_slots(VIT5.layers, k_slots, call + 1)
     torch.cuda.synchronize()
+
+
+def test_complementary_partitions_run_concurrently(gpu_lib):
+    """Encode on 192 CUs and decode on the complementary 64, launched together, overlap: the
+    span from the first start to the last end is well below the two solo times added (the
+    hardware queues of complementary masks sit on different dispatch pipes)."""
+    import dataclasses
+
+    import torch
+
+    import bench
+    nova = gpu_lib
+    vc = dataclasses.replace(synth.VIT_1008, layers=4)
+    lc = dataclasses.replace(synth.LLM_28, layers=2)
+    vit = bench.build_vit(nova, vc, "cuda")
+    llm = bench.build_llm(nova, lc, "cuda")
+    px = torch.from_numpy(synth.image(4, vc.image_h, vc.image_w, seed=1)).to("cuda", torch.bfloat16).contiguous()
+    enc_out = torch.empty(vit.out_shape(4), dtype=torch.bfloat16, device="cuda")
+    ctx = 1500
+    tables, pool = synth.block_tables([ctx + 1] * 8, lc.block, seed=5)
+    kv = nova.KvPool(llm, pool)
+    tab = torch.from_numpy(tables).cuda()
+    ids = torch.from_numpy(synth.text_ids(8, lc.vocab, seed=9)).cuda()
+    pos = torch.full((8,), ctx, dtype=torch.int32, device="cuda")
+    s_e = nova.set_stage_partition(nova.STAGE_ENCODE, nova.make_cu_mask(192, 8))
+    s_d = nova.set_stage_partition(nova.STAGE_DECODE, nova.make_cu_mask(64, 0))
+
+    def encode():
+        vit.encode(px, out=enc_out, stream=s_e)
+
+    def decode(n):
+        for _ in range(n):
+            llm.decode(ids, pos, tab, kv, ctx + 1, stream=s_d)
+
+    def timed(fn, stream):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    t_e = timed(encode, s_e)
+    t_step = timed(lambda: decode(4), s_d) / 4
+    n = max(4, int(round(t_e / t_step)))
+    t_d = timed(lambda: decode(n), s_d)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ev[0].record(s_e)
+    ev[1].record(s_d)
+    encode()
+    decode(n)
+    ev[2].record(s_e)
+    ev[3].record(s_d)
+    torch.cuda.synchronize()
+    start = min(ev[0], ev[1], key=lambda e: ev[0].elapsed_time(e))
+    span = max(start.elapsed_time(ev[2]), start.elapsed_time(ev[3]))
+    print(f"[corun] encode {t_e:.2f} ms, decode x{n} {t_d:.2f} ms, together {span:.2f} ms")
+    assert span < 0.8 * (t_e + t_d)

@@ -154,3 +154,26 @@ def test_poisson_trace_is_seeded_and_bounded():
     assert [r.arrival for r in a] == [r.arrival for r in b]
     assert all(0 < r.arrival < 10 for r in a) and 8 <= len(a) <= 40
     assert all(150 <= r.n_text <= 300 and 16 <= r.n_out <= 48 for r in a)
+
+
+@pytest.mark.parametrize("mode", ["nova", "time_sliced"])
+def test_kv_blocks_taken_at_admission(mode):
+    """KV blocks are taken when a request starts vision encode and returned when it finishes: with
+    a pool that holds two requests at a time, a burst still completes, never holding more."""
+    srv, _ = fake_server(mode)
+    trace = serve.poisson_trace(rate=300.0, window_s=0.05, seed=4, n_text=(5, 9), n_out=(6, 12))
+    need = max(srv._blocks_needed(r) for r in trace)
+    srv.blocks = serve.BlockPool(2 * need)
+    srv.kv.num_blocks = 2 * need
+    seen = []
+    take = srv.blocks.try_take
+
+    def watched(n):
+        got = take(n)
+        seen.append(len(srv.blocks.free))
+        return got
+    srv.blocks.try_take = watched
+    res = srv.run(trace)
+    assert res["requests"] == len(trace) >= 6
+    assert all(len(r.t_tokens) == r.n_out for r in trace)
+    assert min(seen) >= 0 and len(srv.blocks.free) == 2 * need
