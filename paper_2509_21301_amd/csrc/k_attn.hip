@@ -38,8 +38,13 @@ __device__ __forceinline__ float sum_halves(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <typename T, int D, bool CAUSAL>
-__global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
+// NW waves of 32 queries per workgroup (4 for the encoder and the exact mode; 2 for causal
+// prefill, whose per-block work grows with the block index: twice as many, half as heavy
+// workgroups let the heavy blocks spread over the CUs instead of finishing last)
+template <typename T, int D, bool CAUSAL, int NW>
+__global__ void __launch_bounds__(NW * 64, 2) attn_kernel(AttnArgs p) {
+  constexpr int AQB = NW * 32;              // queries per workgroup
+  constexpr int NT = NW * 64;               // threads per workgroup
   constexpr bool F32 = sizeof(T) == 4;
   constexpr int NS = D / 16;                // k-steps of QK^T
   constexpr int DP = (D + 31) / 32 * 32;    // output rows padded to 32
@@ -51,7 +56,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   __shared__ __align__(16) bf16_t vs[NPART][DP * VP];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, lq = lane & 31;
-  const int nqb = (p.sq + AQ - 1) / AQ;
+  const int nqb = (p.sq + AQB - 1) / AQB;
   // one-dimensional grid: workgroups are dealt to the 8 XCDs round-robin, so when the (batch,
   // head) pairs split evenly over the XCDs each XCD takes whole pairs, one after another, and the
   // pair's K and V stay in its L2 while all of the pair's query blocks read them
@@ -72,7 +77,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   }
   const int qb = CAUSAL ? (nqb - 1 - qbi) : qbi;   // heavy causal blocks first
   const int kvh = h / (p.n_q / p.n_kv);
-  const int q0 = qb * AQ;
+  const int q0 = qb * AQB;
   const int qrow = q0 + wave * 32 + lq;
 
   const T* Q = reinterpret_cast<const T*>(p.q) + (size_t)b * p.q_batch + (size_t)h * D;
@@ -103,20 +108,20 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   constexpr int EPC = F32 ? 4 : 8;                     // elements per 16-byte chunk
   constexpr int K_CH = AK * D / EPC;
   constexpr int V_CH = D * AK / EPC;
-  constexpr int K_IT = (K_CH + 255) / 256, V_IT = (V_CH + 255) / 256;
+  constexpr int K_IT = (K_CH + NT - 1) / NT, V_IT = (V_CH + NT - 1) / NT;
   u32x4 rk[K_IT], rv[V_IT];
   // loads are unconditional (chunk index and key row clamped) so that the waits for them stay
   // exact; the surplus chunks are never stored and keys past sk are masked
   auto load_tile = [&](int kv0) {
 #pragma unroll
     for (int i = 0; i < K_IT; ++i) {
-      const int c = min(tid + i * 256, K_CH - 1);
+      const int c = min(tid + i * NT, K_CH - 1);
       const int r = c / (D / EPC), col = (c % (D / EPC)) * EPC;
       rk[i] = *reinterpret_cast<const u32x4*>(K + (size_t)min(kv0 + r, p.sk - 1) * p.k_row + col);
     }
 #pragma unroll
     for (int i = 0; i < V_IT; ++i) {
-      const int c = min(tid + i * 256, V_CH - 1);
+      const int c = min(tid + i * NT, V_CH - 1);
       const int r = c / (AK / EPC), col = (c % (AK / EPC)) * EPC;
       rv[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)r * p.sk_pad + kv0 + col);
     }
@@ -128,7 +133,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   auto store_tile = [&]() {
 #pragma unroll
     for (int i = 0; i < K_IT; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       if (c < K_CH) {
         const int r = c / (D / EPC), col = (c % (D / EPC)) * EPC;
         if constexpr (F32) {
@@ -147,7 +152,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
     }
 #pragma unroll
     for (int i = 0; i < V_IT; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       if (c < V_CH) {
         const int r = c / (AK / EPC), col = (c % (AK / EPC)) * EPC;
         if constexpr (F32) {
@@ -173,7 +178,7 @@ __global__ void __launch_bounds__(256, 2) attn_kernel(AttnArgs p) {
   float m_run = -1e30f, l_run = 0.f;
   const float scale = 1.4426950408889634f / sqrtf((float)D);
 
-  const int kv_end = CAUSAL ? min(p.sk, q0 + AQ) : p.sk;
+  const int kv_end = CAUSAL ? min(p.sk, q0 + AQB) : p.sk;
   const int wave_qmax = q0 + wave * 32 + 31;
   load_tile(0);
   for (int kv0 = 0; kv0 < kv_end; kv0 += AK) {
@@ -645,9 +650,13 @@ static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
       return hipGetLastError();
     }
   }
-  dim3 grid((p.sq + AQ - 1) / AQ * p.n_q * p.batch);
-  if (p.causal) hipLaunchKernelGGL((attn_kernel<T, D, true>), grid, dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((attn_kernel<T, D, false>), grid, dim3(256), 0, s, p);
+  if (p.causal) {
+    constexpr int NW = sizeof(T) == 2 ? 2 : 4;
+    hipLaunchKernelGGL((attn_kernel<T, D, true, NW>), dim3((p.sq + NW * 32 - 1) / (NW * 32) * p.n_q * p.batch),
+                       dim3(NW * 64), 0, s, p);
+  } else {
+    hipLaunchKernelGGL((attn_kernel<T, D, false, 4>), dim3((p.sq + AQ - 1) / AQ * p.n_q * p.batch), dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 
