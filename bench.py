@@ -616,7 +616,7 @@ def main():
     ap.add_argument("--linear-corun", action="store_true",
                     help="only the two-linear co-run study (inter-CU partitions vs intra-CU sharing; prints its JSON)")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
-    ap.add_argument("--profile-stage", choices=["prefill", "decode1", "decode8", "decode32", "copy", "offload"],
+    ap.add_argument("--profile-stage", choices=["prefill", "encode1", "decode1", "decode8", "decode32", "copy", "offload"],
                     help="run only this stage in a loop of --steps passes (for rocprofv3); 'copy' is a plain "
                          "1 GiB device copy that calibrates the HBM byte counters; 'offload' runs only the "
                          "layer-offload comparison")
@@ -681,7 +681,8 @@ def main():
         print(json.dumps(measure_offload(nova, torch, st, ServingSetup(nova, torch, synth, st))), flush=True)
         return
     if args.profile_stage:
-        fn = st.prefill if args.profile_stage == "prefill" else (lambda: st.decode(int(args.profile_stage[6:])))
+        fn = {"prefill": st.prefill, "encode1": lambda: st.encode(1)}.get(
+            args.profile_stage, lambda: st.decode(int(args.profile_stage[6:])))
         for _ in range(args.warmup):
             fn()
         ms = time_passes(torch, fn, args.steps, stream)
@@ -766,7 +767,7 @@ def main():
     for b in (1, 8, 32):
         st.decode(b)
         t = time_passes(torch, lambda: st.decode(b), 10, stream)
-        wb, kvb = decode_bytes(lc, b, st.ctx_max)
+        wb, kvb = decode_bytes(lc, b, st.s + 1)          # every sequence sits at position s: s + 1 keys
         stages[f"decode_b{b}"] = {"ms": round(t, 3), "tok_per_s": round(b / (t / 1e3), 1),
                                   "hbm_gbs": round((wb + kvb) / (t / 1e3) / 1e9, 1),
                                   "hbm_frac": round((wb + kvb) / (t / 1e3) / 1e9 / HBM_PEAK_GBS, 3)}
