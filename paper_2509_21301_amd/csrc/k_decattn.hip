@@ -9,6 +9,11 @@
 //    tokens reads 8 contiguous bytes per lane);
 //  * the per-head max and sum over tokens are wavefront shuffles (lane ^ 16, lane ^ 32);
 //    waves are merged through LDS and splits by a second pass (log-sum-exp combine).
+// The step's own token is folded in: the kernel sums the QKV projection's split-K slabs, applies
+// the rotary embedding to q and k (the sines and cosines of the sequence's position come from a
+// table the step computes once for all layers), and the wave whose block pair holds that
+// position appends k and v to the cache and uses them in place of the slot's old contents.
+// So no rotary/append pass runs between the QKV projection and the attention.
 // K pool layout: [num_blocks][n_kv][16][D];  V pool layout: [num_blocks][n_kv][D][16].
 #include "common.hpp"
 #include "kernels.hpp"
@@ -45,15 +50,20 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) d
   constexpr int NS = D / 32;      // k-steps of S = K Q^T
   constexpr int ND = D / 16;      // output row blocks of O^T
   using Pair = DaPair<F32, NS, ND>;
+  constexpr int HALF = D / 2;
   __shared__ float sm_m[4][16], sm_l[4][16];
   __shared__ float sm_o[4][D][16];
+  __shared__ __align__(16) T sm_q[16][D];        // the step's rotated q of the group's heads
+  __shared__ __align__(16) T sm_nk[D];           // the new token's rotated k and its v
+  __shared__ T sm_nv[D];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int G = p.n_q / p.n_kv;
   const int col = lane & 15, grp = lane >> 4;
-  const int ctx = p.pos[b] + 1;
+  const int ps = p.pos[b];
+  const int ctx = ps + 1;
   const int nblk = (ctx + DA_BLOCK - 1) / DA_BLOCK;
   const int pair_begin = split * pairs_per_split;
   const int pair_end = min(pair_begin + pairs_per_split, (nblk + 1) / 2);
@@ -63,6 +73,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) d
   // this wave takes pairs first, first + 4, ...: iteration it covers pair first + 4 it
   const int first = pair_begin + wave;
   const int n_it = first < pair_end ? (pair_end - first + 3) / 4 : 0;
+  // the new token (position ps) is slot ps % 16 of block ps / 16, in the context's last pair;
+  // it_new: this wave's iteration over that pair (-1: another wave's)
+  const int new_blk = ps / DA_BLOCK, slot = ps % DA_BLOCK;
+  const int new_pair = new_blk / 2, jn = new_blk & 1;
+  const int it_new = new_pair >= first && new_pair < pair_end && ((new_pair - first) & 3) == 0 ? (new_pair - first) >> 2 : -1;
 
   // block-table entries of 32 iterations at a time, one per lane (lane 2i + j: block j of
   // iteration i), read back with a uniform lane index, so the K/V loads of a pair wait for no
@@ -102,25 +117,129 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) d
     }
   };
 
+  // two register sets: the loads of the next pair are in flight while this pair is computed
+  Pair ra, rb;
+  if (n_it > 0) load(0, ra);
+
+  // The step's q for the G heads of this group and, in the workgroup whose splits hold the new
+  // token, its k and v: the projection's split-K slabs summed in order, q and k rotated (dim c <
+  // D/2 pairs with c + D/2), staged in LDS in the activation type.  Every load is requested before
+  // any is summed (4 slabs at a time), so this costs one round trip to memory, taken while the
+  // first K/V loads are in flight.  Thread t takes rotation pairs t, t + 256, ... (head h = pair /
+  // (D/2), h == G: the new k) and, when t < D, dimension t of the new v.
+  const bool owner_wg = new_pair >= pair_begin && new_pair < pair_end;
+  {
+    constexpr int PPT = (17 * HALF + 255) / 256;      // pairs per thread at most (G <= 16, plus k)
+    const int npairs = (G + (owner_wg ? 1 : 0)) * HALF;
+    const size_t qkvw = (size_t)(p.n_q + 2 * p.n_kv) * D;
+    int off[PPT];
+    float sn[PPT], cs[PPT], a1[PPT], a2[PPT], av = 0.f;
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+      const int pi = min(tid + 256 * u, npairs - 1);        // clamped: the duplicates are not stored
+      const int h = pi / HALF, c = pi % HALF;
+      off[u] = (h < G ? kvh * G + h : p.n_q + kvh) * D + c;
+      sn[u] = p.rope[(size_t)b * D + c];
+      cs[u] = p.rope[(size_t)b * D + HALF + c];
+      a1[u] = a2[u] = 0.f;
+    }
+    const int voff = (p.n_q + p.n_kv + kvh) * D + (tid % D);
+    for (int sp0 = 0; sp0 < p.qkv_splits; sp0 += 4) {
+      float t1[4][PPT], t2[4][PPT], tv[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float* r = p.qkv + ((size_t)min(sp0 + q, p.qkv_splits - 1) * p.B + b) * qkvw;
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+          t1[q][u] = r[off[u]];
+          t2[q][u] = r[off[u] + HALF];
+        }
+        tv[q] = r[voff];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (sp0 + q < p.qkv_splits) {
+#pragma unroll
+          for (int u = 0; u < PPT; ++u) { a1[u] += t1[q][u]; a2[u] += t2[q][u]; }
+          av += tv[q];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+      const int pi = tid + 256 * u;
+      if (pi >= npairs) break;
+      const int h = pi / HALF, c = pi % HALF;
+      const float y1 = a1[u] * cs[u] - a2[u] * sn[u], y2 = a2[u] * cs[u] + a1[u] * sn[u];
+      T* dst = h < G ? sm_q[h] : sm_nk;
+      dst[c] = from_f<T>(y1);
+      dst[c + HALF] = from_f<T>(y2);
+    }
+    if (owner_wg && tid < D) sm_nv[tid] = from_f<T>(av);
+  }
+  __syncthreads();
+
   // Q^T fragments: head col of this group, dims 32s + 8grp .. +8 (zero for col >= G)
   Frag8 qh[NS], ql[F32 ? NS : 1];
-  const T* qsrc = reinterpret_cast<const T*>(p.q) + ((size_t)b * p.n_q + kvh * G + col) * D;
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     if (col < G) {
+      const T* qs = sm_q[col] + 32 * s + 8 * grp;
       if constexpr (F32) {
         float x[8];
-        *reinterpret_cast<float4*>(x) = *reinterpret_cast<const float4*>(qsrc + 32 * s + 8 * grp);
-        *reinterpret_cast<float4*>(x + 4) = *reinterpret_cast<const float4*>(qsrc + 32 * s + 8 * grp + 4);
+        *reinterpret_cast<float4*>(x) = *reinterpret_cast<const float4*>(qs);
+        *reinterpret_cast<float4*>(x + 4) = *reinterpret_cast<const float4*>(qs + 4);
         split8(x, qh[s], ql[s]);
       } else {
-        qh[s] = *reinterpret_cast<const Frag8*>(qsrc + 32 * s + 8 * grp);
+        qh[s] = *reinterpret_cast<const Frag8*>(qs);
       }
     } else {
       qh[s] = zero_frag();
       if constexpr (F32) ql[s] = zero_frag();
     }
   }
+  // the new token appended to the cache (K row, V^T column)
+  if (owner_wg && tid < D) {
+    const size_t base = ((size_t)table[new_blk] * p.n_kv + kvh) * DA_BLOCK * D;
+    const_cast<T*>(kpool)[base + (size_t)slot * D + tid] = sm_nk[tid];
+    const_cast<T*>(vpool)[base + (size_t)tid * DA_BLOCK + slot] = sm_nv[tid];
+  }
+  // the owner wave's registers of block jn take the new token, whatever the cache held there
+  // (jn and slot are uniform: the branches select registers, they do not index them)
+  auto patch = [&](Pair& r) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (j != jn) continue;
+      if (col == slot) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          if constexpr (F32) {
+            r.k[j][s][0] = *reinterpret_cast<const float4*>(sm_nk + 32 * s + 8 * grp);
+            r.k[j][s][1] = *reinterpret_cast<const float4*>(sm_nk + 32 * s + 8 * grp + 4);
+          } else {
+            r.k[j][s] = *reinterpret_cast<const Frag8*>(sm_nk + 32 * s + 8 * grp);
+          }
+        }
+      }
+      if (grp == slot / 4) {
+        const int e = slot & 3;
+#pragma unroll
+        for (int i = 0; i < ND; ++i) {
+          const T v = sm_nv[16 * i + col];
+          if constexpr (F32) {
+            if (e == 0) r.v[i][j].x = v;
+            else if (e == 1) r.v[i][j].y = v;
+            else if (e == 2) r.v[i][j].z = v;
+            else r.v[i][j].w = v;
+          } else {
+            const uint32_t keep = (e & 1) ? 0x0000ffffu : 0xffff0000u;
+            const uint32_t put = (uint32_t)v << (16 * (e & 1));
+            if (e < 2) r.v[i][j].x = (r.v[i][j].x & keep) | put;
+            else r.v[i][j].y = (r.v[i][j].y & keep) | put;
+          }
+        }
+      }
+    }
+  };
 
   f32x4 o[ND];
 #pragma unroll
@@ -228,14 +347,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) d
     }
   };
 
-  // two register sets: the loads of the next pair are in flight while this pair is computed
-  Pair ra, rb;
-  if (n_it > 0) load(0, ra);
   for (int it = 0; it < n_it; it += 2) {
     if (it + 1 < n_it) load(it + 1, rb);
+    if (it == it_new) patch(ra);
     compute(it, ra);
     if (it + 1 >= n_it) break;
     if (it + 2 < n_it) load(it + 2, ra);
+    if (it + 1 == it_new) patch(rb);
     compute(it + 1, rb);
   }
 
@@ -297,6 +415,7 @@ __global__ void __launch_bounds__(D) dec_attn_combine(DecAttnArgs p, int nsplit)
 template <typename T, int D>
 static hipError_t dec_launch(const DecAttnArgs& p, hipStream_t s) {
   const int nsplit = dec_splits(p.B, p.n_kv, p.max_ctx);
+  if (nsplit > 1 && p.partial == nullptr) return hipErrorInvalidValue;
   const int pairs = (p.max_ctx + 31) / 32;
   const int per = (pairs + nsplit - 1) / nsplit;
   hipLaunchKernelGGL((dec_attn_kernel<T, D>), dim3(nsplit, p.n_kv, p.B), dim3(256), 0, s, p, per);
@@ -309,7 +428,8 @@ static hipError_t dec_launch(const DecAttnArgs& p, hipStream_t s) {
 template <typename T>
 hipError_t decode_attention(const DecAttnArgs& p, int head_dim, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  if (p.block != DA_BLOCK || p.n_kv <= 0 || p.n_q % p.n_kv || p.n_q / p.n_kv > 16 || p.max_ctx <= 0)
+  if (p.block != DA_BLOCK || p.n_kv <= 0 || p.n_q % p.n_kv || p.n_q / p.n_kv > 16 || p.max_ctx <= 0 ||
+      p.qkv == nullptr || p.qkv_splits <= 0)
     return hipErrorInvalidValue;
   switch (head_dim) {
     case 64: return dec_launch<T, 64>(p, s);

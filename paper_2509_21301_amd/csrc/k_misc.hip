@@ -238,64 +238,6 @@ hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ decode QKV: rotate, store q, append k/v
-template <typename T>
-__global__ void qkv_decode_kernel(const float* __restrict__ qkv, int splits, int B, int n_q, int n_kv, int D, float theta,
-                                  const int* __restrict__ pos, T* __restrict__ qout, T* __restrict__ kpool,
-                                  T* __restrict__ vpool, const int* __restrict__ tables, int max_blocks, int block) {
-  const int half = D / 2;
-  const int heads = n_q + 2 * n_kv;
-  const long total = (long)B * heads * half;
-  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
-    const int c = (int)(idx % half);
-    const int hh = (int)((idx / half) % heads);
-    const int b = (int)(idx / ((long)half * heads));
-    const int ps = pos[b];
-    float x1 = 0.f, x2 = 0.f;
-#pragma unroll 4
-    for (int sp = 0; sp < splits; ++sp) {
-      const float* e = qkv + ((size_t)sp * B + b) * heads * D + (size_t)hh * D;
-      x1 += e[c];
-      x2 += e[c + half];
-    }
-    if (hh < n_q + n_kv) {
-      float sn, cs;
-      rope_sincos(ps, c, D, theta, &sn, &cs);
-      const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
-      x1 = y1; x2 = y2;
-    }
-    if (hh < n_q) {
-      T* q = qout + ((size_t)b * n_q + hh) * D;
-      q[c] = from_f<T>(x1);
-      q[c + half] = from_f<T>(x2);
-      continue;
-    }
-    const int phys = tables[(size_t)b * max_blocks + ps / block], slot = ps % block;
-    if (hh < n_q + n_kv) {
-      const int kvh = hh - n_q;
-      T* k = kpool + (((size_t)phys * n_kv + kvh) * block + slot) * D;
-      k[c] = from_f<T>(x1);
-      k[c + half] = from_f<T>(x2);
-    } else {
-      const int kvh = hh - n_q - n_kv;
-      T* v = vpool + ((size_t)phys * n_kv + kvh) * D * block;
-      v[(size_t)c * block + slot] = from_f<T>(x1);
-      v[(size_t)(c + half) * block + slot] = from_f<T>(x2);
-    }
-  }
-}
-
-template <typename T>
-hipError_t qkv_decode(const float* qkv, int splits, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos,
-                      T* qout, T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s) {
-  if (B <= 0) return hipSuccess;
-  const long total = (long)B * (n_q + 2 * n_kv) * (D / 2);
-  const int grid = (int)std::min<long>((total + 255) / 256, 65536);
-  hipLaunchKernelGGL((qkv_decode_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, splits, B, n_q, n_kv, D, rope_theta, pos, qout,
-                     kpool, vpool, tables, max_blocks, block);
-  return hipGetLastError();
-}
-
 // ------------------------------------------------------------------ decode residual + RMSNorm
 // One 1024-thread workgroup per row: fold the split-K partials of the previous projection into
 // the fp32 residual stream, then normalise the row for the next projection.
@@ -426,7 +368,9 @@ __global__ void __launch_bounds__(256) decode_embed_kernel(const int* __restrict
                                                            int H, const bf16_t* __restrict__ g, float* __restrict__ x,
                                                            T* __restrict__ a, float* __restrict__ ss0, int ss_parts,
                                                            unsigned long long* __restrict__ keys,
-                                                           unsigned* __restrict__ counters, int n_counters) {
+                                                           unsigned* __restrict__ counters, int n_counters,
+                                                           const int* __restrict__ pos, float theta, int D,
+                                                           float* __restrict__ rope) {
   __shared__ float red[4];
   const int b = blockIdx.x, B = gridDim.x;
   const bf16_t* e = embed + (size_t)ids[b] * H;
@@ -445,22 +389,30 @@ __global__ void __launch_bounds__(256) decode_embed_kernel(const int* __restrict
   if (threadIdx.x == 0) keys[b] = 0ull;
   if (b == 0)
     for (int i = threadIdx.x; i < n_counters; i += 256) counters[i] = 0u;
+  // the rotary sines and cosines at this step's position, shared by every layer
+  for (int c = threadIdx.x; c < D / 2; c += 256) {
+    float sn, cs;
+    rope_sincos(pos[b], c, D, theta, &sn, &cs);
+    rope[(size_t)b * D + c] = sn;
+    rope[(size_t)b * D + D / 2 + c] = cs;
+  }
   __syncthreads();
   if (threadIdx.x == 0) ss0[b] = red[0] + red[1] + red[2] + red[3];
 }
 
 template <typename T>
 hipError_t decode_embed(const int* ids, int B, const bf16_t* embed, int H, const bf16_t* g, float* x, T* a, float* ss0,
-                        int ss_parts, unsigned long long* keys, unsigned* counters, int n_counters, hipStream_t s) {
+                        int ss_parts, unsigned long long* keys, unsigned* counters, int n_counters, const int* pos,
+                        float theta, int D, float* rope, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   hipLaunchKernelGGL((decode_embed_kernel<T>), dim3(B), dim3(256), 0, s, ids, embed, H, g, x, a, ss0, ss_parts, keys,
-                     counters, n_counters);
+                     counters, n_counters, pos, theta, D, rope);
   return hipGetLastError();
 }
 template hipError_t decode_embed<bf16_t>(const int*, int, const bf16_t*, int, const bf16_t*, float*, bf16_t*, float*, int,
-                                         unsigned long long*, unsigned*, int, hipStream_t);
+                                         unsigned long long*, unsigned*, int, const int*, float, int, float*, hipStream_t);
 template hipError_t decode_embed<float>(const int*, int, const bf16_t*, int, const bf16_t*, float*, float*, float*, int,
-                                        unsigned long long*, unsigned*, int, hipStream_t);
+                                        unsigned long long*, unsigned*, int, const int*, float, int, float*, hipStream_t);
 
 // ------------------------------------------------------------------ CU placement probe
 __global__ void cu_probe_kernel(uint32_t* __restrict__ out, int n) {
@@ -540,8 +492,6 @@ template hipError_t zero_tail_cols<float>(float*, long, int, int, hipStream_t);
 
 template hipError_t qkv_prefill<bf16_t>(bf16_t*, int, int, int, int, int, float, int, bf16_t*, int, bf16_t*, bf16_t*, const int*, int, hipStream_t);
 template hipError_t qkv_prefill<float>(float*, int, int, int, int, int, float, int, float*, int, float*, float*, const int*, int, hipStream_t);
-template hipError_t qkv_decode<bf16_t>(const float*, int, int, int, int, int, float, const int*, bf16_t*, bf16_t*, bf16_t*, const int*, int, int, hipStream_t);
-template hipError_t qkv_decode<float>(const float*, int, int, int, int, int, float, const int*, float*, float*, float*, const int*, int, int, hipStream_t);
 template hipError_t resid_rmsnorm<bf16_t>(const float*, int, float*, int, int, const bf16_t*, float, bf16_t*, int, unsigned long long*, hipStream_t);
 template hipError_t resid_rmsnorm<float>(const float*, int, float*, int, int, const bf16_t*, float, float*, int, unsigned long long*, hipStream_t);
 template hipError_t resid_fold<bf16_t>(const float*, int, float*, int, int, const bf16_t*, bf16_t*, int, float*,

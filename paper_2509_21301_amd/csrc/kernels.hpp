@@ -98,13 +98,15 @@ hipError_t attention(const AttnArgs& p, int head_dim, hipStream_t s);
 
 // Paged decode attention: one query per sequence against its paged KV blocks.
 struct DecAttnArgs {
-  const void* q;              // [B, n_q, D]
-  const void* kpool;          // [num_blocks, n_kv, block, D] for this layer
-  const void* vpool;
+  const float* qkv;           // QKV projection, fp32 [qkv_splits][B][(n_q + 2 n_kv) D]: split-K slabs,
+  int qkv_splits;             //   summed and rotated here (q and k at pos)
+  const float* rope;          // [B][2][D/2]: sines, then cosines of each sequence's position
+  void* kpool;                // [num_blocks, n_kv, block, D] for this layer; the step's k is appended
+  void* vpool;                // [num_blocks, n_kv, D, block]; the step's v is appended
   const int* tables; int max_blocks;
   const int* pos;             // query position; context = pos + 1
   void* out;                  // [B, n_q * D]
-  float* partial;             // workspace
+  float* partial;             // workspace: split partials
   int B, n_q, n_kv, block, max_ctx;
 };
 size_t dec_attn_partial_floats(int B, int n_q, int D, int max_ctx, int n_kv);
@@ -135,11 +137,6 @@ hipError_t zero_tail_cols(T* buf, long rows, int ld, int c0, hipStream_t s);
 template <typename T>
 hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0,
                        T* vt, int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s);
-// Decode: qkv = sum over `splits` fp32 slabs [splits][B][(n_q+2n_kv)D] (1 slab: the projection
-// itself); rotate at pos[b]; q -> qout [B, n_q, D]; k, v -> paged cache.
-template <typename T>
-hipError_t qkv_decode(const float* qkv, int splits, int B, int n_q, int n_kv, int D, float rope_theta, const int* pos,
-                      T* qout, T* kpool, T* vpool, const int* tables, int max_blocks, int block, hipStream_t s);
 // Decode residual + RMSNorm, one workgroup per row: x[b] += sum_s partial[s][b] (if splits > 0),
 // then a[b] = x[b] / sqrt(mean(x[b]^2) + eps) * g.
 // keys != null: also zero keys[b] for the fused argmax of the projection that follows.
@@ -157,10 +154,12 @@ hipError_t argmax_finish(const unsigned long long* keys, int B, int* ids, hipStr
 // x[r] = r < n_vis ? vis[r] : embed[ids[r - n_vis]]  (fp32 out)
 // Decode step start: x[b] = embed[ids[b]] (fp32), a[b] = x[b] * g in the activation type;
 // ss0[0 * B + b] = sum of squares of x[b] and ss0[t * B + b] = 0 for 0 < t < ss_parts; zeroes
-// keys[B] and counters[n_counters].
+// keys[B] and counters[n_counters]; rope[b] = the rotary sines then cosines of position pos[b]
+// (2 x D/2 floats), which every layer's decode attention reads.
 template <typename T>
 hipError_t decode_embed(const int* ids, int B, const bf16_t* embed, int H, const bf16_t* g, float* x, T* a, float* ss0,
-                        int ss_parts, unsigned long long* keys, unsigned* counters, int n_counters, hipStream_t s);
+                        int ss_parts, unsigned long long* keys, unsigned* counters, int n_counters, const int* pos,
+                        float theta, int D, float* rope, hipStream_t s);
 template <typename T>
 hipError_t embed_rows(const T* vis, int n_vis, const int* ids, int n_ids, const bf16_t* embed, int H, float* x,
                       hipStream_t s);

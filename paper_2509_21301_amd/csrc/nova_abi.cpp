@@ -595,12 +595,12 @@ struct DecodeBufs {
   float* x;                   // residual stream [B][H]
   T* a;                       // x times the next RMSNorm's gain, input of the next projection [B][H]
   float* qkv;                 // QKV projection (fp32) when not split
-  T* q;                       // rotated queries
   T* att;                     // attention output
   T* hm;                      // MLP hidden
   unsigned long long* keys;   // greedy argmax keys
   float* ss;                  // per-tile row sums of squares of the 2 L + 1 fused RMSNorms [2L+1][H/64][B]
   unsigned* counters;         // split-K arrival counters of the O and down projections [2L][H/64]
+  float* rope;                // rotary sines and cosines of each sequence's position [B][2][D/2]
   float* part;                // split-K partials
   float* apart;               // decode-attention split partials
   size_t used;
@@ -617,12 +617,12 @@ DecodeBufs<T> decode_bufs(const nova_llm* m, int B, int max_ctx, void* base) {
   d.x = w.take<float>((size_t)B * H);
   d.a = w.take<T>((size_t)B * H);
   d.qkv = w.take<float>((size_t)B * m->qkvw);
-  d.q = w.take<T>((size_t)B * qd);
   d.att = w.take<T>((size_t)B * qd);
   d.hm = w.take<T>((size_t)B * m->ip);
   d.keys = w.take<unsigned long long>((size_t)B);
   d.ss = w.take<float>((size_t)(2 * c.layers + 1) * (H / 64) * B);
   d.counters = w.take<unsigned>((size_t)2 * c.layers * (H / 64));
+  d.rope = w.take<float>((size_t)B * c.head_dim);
   size_t part = 0;
   const bool f32 = sizeof(T) == 4;
   part = std::max(part, nova::gemv_partial_floats(B, m->qkvw, c.hidden, f32, g.cus));
@@ -734,9 +734,8 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
   auto attention_block = [&](int l) -> int {
     T* kp = (T*)kv->k + l * kv_layer;
     T* vp = (T*)kv->v + l * kv_layer;
-    CALL(NOVA_KIND_MISC, s, nova::qkv_decode<T>(sp_qkv > 1 ? d.part : d.qkv, sp_qkv, B, c.n_q, c.n_kv, D, c.rope_theta, pos,
-                                                 d.q, kp, vp, tables, max_blocks, c.block, s));
-    nova::DecAttnArgs p{d.q, kp, vp, tables, max_blocks, pos, d.att, d.apart, B, c.n_q, c.n_kv, c.block, max_ctx};
+    nova::DecAttnArgs p{sp_qkv > 1 ? d.part : d.qkv, sp_qkv, d.rope, kp, vp, tables, max_blocks, pos, d.att, d.apart,
+                        B, c.n_q, c.n_kv, c.block, max_ctx};
     CALL(NOVA_KIND_DECODE_ATTN, s, nova::decode_attention<T>(p, D, s));
     return (int)NOVA_OK;
   };
@@ -746,11 +745,12 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
     // (embedding, O and down projections) writes x times the norm's gain and per-tile sums of
     // squares of x, and the consumer projection (QKV, gate/up, LM head) scales each output by the
     // row's rsqrt.  (With larger batches the split-K tail of the producers outgrows a separate
-    // norm kernel.)  The QKV split-K partials are summed by the rotary/KV-append kernel.
+    // norm kernel.)  The QKV split-K partials are summed by the decode attention, which also
+    // applies the rotary embedding and appends the new k and v to the cache.
     auto ss = [&](int k) { return d.ss + (size_t)k * tiles * B; };
     CALL(NOVA_KIND_MISC, s, nova::decode_embed<T>(ids, B, (const bf16_t*)m->d.embed, H,
                                                   c.layers > 0 ? layer_w(0, 0) : final_gain, d.x, d.a, ss(0), tiles, d.keys,
-                                                  d.counters, 2 * c.layers * tiles, s));
+                                                  d.counters, 2 * c.layers * tiles, pos, c.rope_theta, D, d.rope, s));
     for (int l = 0; l < c.layers; ++l) {
       auto W = [&](int i) { return layer_w(l, i); };
       {
@@ -794,7 +794,7 @@ int llm_decode_t(const nova_llm* m, const int* ids, const int* pos, const int* t
     auto ss = [&](int k) { return d.ss + (size_t)k * tiles * B; };
     CALL(NOVA_KIND_MISC, s, nova::decode_embed<T>(ids, B, (const bf16_t*)m->d.embed, H,
                                                   c.layers > 0 ? layer_w(0, 0) : final_gain, d.x, d.a, ss(0), tiles, d.keys,
-                                                  nullptr, 0, s));
+                                                  nullptr, 0, pos, c.rope_theta, D, d.rope, s));
     for (int l = 0; l < c.layers; ++l) {
       auto W = [&](int i) { return layer_w(l, i); };
       {
