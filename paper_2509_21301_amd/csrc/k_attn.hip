@@ -384,10 +384,15 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   // dispatched first; each of their waves takes one query group and one 32-key half of every tile.
   const bool has_light = p.sq % AQW != 0 && p.sq % AQW <= 64;
   const int pairs = p.batch * p.n_q;
+  // key range: with kv_parts > 1, workgroup blockIdx.x takes range blockIdx.x / (workgroups of
+  // one range) of whole 64-key tiles, the same (query block, head) layout in every range
+  const int kpart = blockIdx.x / (nqb * pairs);
+  const int tpp = ((p.sk + AK - 1) / AK + p.kv_parts - 1) / p.kv_parts;
+  const int kbeg = min(kpart * tpp * AK, p.sk), kend = min((kpart + 1) * tpp * AK, p.sk);
   int qb, h, b;
   bool light = false;
   {
-    const int lin = blockIdx.x;
+    const int lin = blockIdx.x - kpart * nqb * pairs;
     int pair;
     if (has_light && lin < pairs) {
       light = true;
@@ -417,6 +422,17 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   const bf16_t* VT = reinterpret_cast<const bf16_t*>(p.vt) + ((size_t)b * p.n_kv + kvh) * D * (size_t)p.sk_pad;
 
   const float scale = 1.4426950408889634f / sqrtf((float)D);
+  // where a query row's normalised output goes: the output itself, or with several key ranges
+  // this range's partial row (bf16, [range][pair][query][D]) and its (max, sum) (fp32 pairs after
+  // all partial rows), written by the lanes of the first half
+  auto out_row = [&](int bb, int hh, int qrow, float m, float lsum) -> bf16_t* {
+    if (p.kv_parts == 1)
+      return reinterpret_cast<bf16_t*>(p.out) + (size_t)bb * p.o_batch + (size_t)qrow * p.o_row + (size_t)hh * D;
+    const size_t row = ((size_t)kpart * pairs + (size_t)bb * p.n_q + hh) * p.sq + qrow;
+    bf16_t* po = reinterpret_cast<bf16_t*>(p.part);
+    if (g == 0) reinterpret_cast<float2*>(po + (size_t)p.kv_parts * pairs * p.sq * D)[row] = make_float2(m, lsum);
+    return po + row * D;
+  };
   // DMA instruction i (dealt to wave i % 4) fills LDS slots 64 i .. 64 i + 63 of a tile, slot j
   // being piece j % (slots per row) of LDS row j / (slots per row); pad slots are masked off
   int k_row[K_IW], k_col[K_IW], v_off[V_IW];
@@ -476,16 +492,16 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
           vf[tt][c] = *reinterpret_cast<const Frag8*>(&vs[(c * 32 + lq) * VP + kb * 32 + 16 * tt + 8 * g]);
       light_step<D, NS, NC, ONES>(q1, kf, vf, kv0 + 32 * kb, p.sk, g, scale, o1, m1, l1);
     };
-    dma(0, ks0, vs0);
+    dma(kbeg, ks0, vs0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int kv0 = 0; kv0 < p.sk; kv0 += 2 * AK) {
-      if (kv0 + AK < p.sk) dma(kv0 + AK, ks1, vs1);
+    for (int kv0 = kbeg; kv0 < kend; kv0 += 2 * AK) {
+      if (kv0 + AK < kend) dma(kv0 + AK, ks1, vs1);
       if (lact) ltile(kv0, ks0, vs0);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      if (kv0 + AK >= p.sk) break;
-      if (kv0 + 2 * AK < p.sk) dma(kv0 + 2 * AK, ks0, vs0);
+      if (kv0 + AK >= kend) break;
+      if (kv0 + 2 * AK < kend) dma(kv0 + 2 * AK, ks0, vs0);
       if (lact) ltile(kv0 + AK, ks1, vs1);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
@@ -512,8 +528,9 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o1[c][r] = o1[c][r] * f1 + cb[(c * 16 + r) * 64 + lane] * f2;
-    const float inv = 1.0f / (ONES ? o1[NC - 1][8] : l1 * f1 + l2 * f2);
-    bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + (size_t)b * p.o_batch + (size_t)qrow * p.o_row + (size_t)h * D;
+    const float lsum = ONES ? o1[NC - 1][8] : l1 * f1 + l2 * f2;
+    const float inv = 1.0f / lsum;
+    bf16_t* out = out_row(b, h, qrow, mm, lsum);
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -606,16 +623,16 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
     }
   };
 
-  dma(0, ks0, vs0);
+  dma(kbeg, ks0, vs0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  for (int kv0 = 0; kv0 < p.sk; kv0 += 2 * AK) {
-    if (kv0 + AK < p.sk) dma(kv0 + AK, ks1, vs1);
+  for (int kv0 = kbeg; kv0 < kend; kv0 += 2 * AK) {
+    if (kv0 + AK < kend) dma(kv0 + AK, ks1, vs1);
     if (active) tile(kv0, ks0, vs0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (kv0 + AK >= p.sk) break;
-    if (kv0 + 2 * AK < p.sk) dma(kv0 + 2 * AK, ks0, vs0);
+    if (kv0 + AK >= kend) break;
+    if (kv0 + 2 * AK < kend) dma(kv0 + 2 * AK, ks0, vs0);
     if (active) tile(kv0 + AK, ks1, vs1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -626,8 +643,9 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
     const int qrow = qbase + 32 * u + lq;
     if (qrow >= p.sq) continue;
     // with ONES, element 8 of the last block is output row 32 (NC - 1) + 16 + 4 g: a ones row
-    const float inv = 1.0f / (ONES ? o[u][NC - 1][8] : l_run[u]);
-    bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + (size_t)b * p.o_batch + (size_t)qrow * p.o_row + (size_t)h * D;
+    const float lsum = ONES ? o[u][NC - 1][8] : l_run[u];
+    const float inv = 1.0f / lsum;
+    bf16_t* out = out_row(b, h, qrow, m_run[u], lsum);
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -640,11 +658,86 @@ __global__ void __launch_bounds__(256, 2) attn_wide_kernel(AttnArgs p) {
   }
 }
 
+// Merge of the key ranges of attn_wide_kernel: thread (pair, query, 8 dims) weighs each range's
+// normalised partial by exp2((m_r - max) scale) times its probability sum and divides by the
+// weights' total; all ranges' loads are issued before any is used.
+template <int D>
+__global__ void __launch_bounds__(256) attn_merge_kernel(AttnArgs p) {
+  constexpr int CH = D / 8;
+  const int pairs = p.batch * p.n_q;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)pairs * p.sq * CH) return;
+  const int ch = (int)(idx % CH);
+  const long r = idx / CH;
+  const int qrow = (int)(r % p.sq), pair = (int)(r / p.sq);
+  const int h = pair % p.n_q, b = pair / p.n_q;
+  const bf16_t* po = reinterpret_cast<const bf16_t*>(p.part);
+  const float2* st = reinterpret_cast<const float2*>(po + (size_t)p.kv_parts * pairs * p.sq * D);
+  const float scale = 1.4426950408889634f / sqrtf((float)D);
+  float2 ml[3];
+  Frag8 v[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const size_t row = ((size_t)min(k, p.kv_parts - 1) * pairs + pair) * p.sq + qrow;
+    ml[k] = st[row];
+    v[k] = *reinterpret_cast<const Frag8*>(po + row * D + 8 * ch);
+  }
+  float mx = ml[0].x;
+#pragma unroll
+  for (int k = 1; k < 3; ++k)
+    if (k < p.kv_parts) mx = fmaxf(mx, ml[k].x);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, wsum = 0.f;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    if (k >= p.kv_parts) break;
+    const float w = __builtin_amdgcn_exp2f((ml[k].x - mx) * scale) * ml[k].y;
+    wsum += w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += w * __uint_as_float(v[k].w[e] << 16);
+      acc[2 * e + 1] += w * __uint_as_float(v[k].w[e] & 0xffff0000u);
+    }
+  }
+  const float inv = 1.0f / wsum;
+  Frag8 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o.w[e] = pack2(acc[2 * e] * inv, acc[2 * e + 1] * inv);
+  *reinterpret_cast<Frag8*>(reinterpret_cast<bf16_t*>(p.out) + (size_t)b * p.o_batch + (size_t)qrow * p.o_row +
+                            (size_t)h * D + 8 * ch) = o;
+}
+
+// Key ranges for the wide kernel: 2 or 3 when that fills the workgroup slots (2 per CU) at least
+// 15 points better than one range (one 1008x1008 image: 336 workgroups leave a third of 512 slots
+// empty; 3 ranges make 1008 of 1024), each range at least 8 tiles, and the scratch holds the
+// partial rows.
+static int wide_kv_parts(const AttnArgs& p, int D) {
+  if (p.part == nullptr) return 1;
+  const long wgs = (long)((p.sq + AQW - 1) / AQW) * p.n_q * p.batch;
+  const long slots = 2L * (p.cus > 0 ? p.cus : 256);
+  auto eff = [&](long u) { return (double)u / (double)(((u + slots - 1) / slots) * slots); };
+  const int nkt = (p.sk + AK - 1) / AK;
+  int best = 1;
+  double best_eff = eff(wgs) + 0.15;
+  for (int k = 2; k <= 3; ++k) {
+    const size_t need = (size_t)k * p.batch * p.n_q * p.sq * (2 * D + 8);
+    if (nkt < 8 * k || need > p.part_bytes) continue;
+    if (eff(wgs * k) > best_eff + 1e-9) { best = k; best_eff = eff(wgs * k); }
+  }
+  return best;
+}
+
 template <typename T, int D>
 static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
   if constexpr (sizeof(T) == 2 && D <= 80) {
     if (!p.causal) {
-      hipLaunchKernelGGL((attn_wide_kernel<D>), dim3((p.sq + AQW - 1) / AQW * p.n_q * p.batch), dim3(256), 0, s, p);
+      AttnArgs q = p;
+      q.kv_parts = wide_kv_parts(p, D);
+      const int wgs = (p.sq + AQW - 1) / AQW * p.n_q * p.batch;
+      hipLaunchKernelGGL((attn_wide_kernel<D>), dim3(wgs * q.kv_parts), dim3(256), 0, s, q);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess || q.kv_parts == 1) return e;
+      const long n = (long)p.batch * p.n_q * p.sq * (D / 8);
+      hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, q);
       return hipGetLastError();
     }
   }

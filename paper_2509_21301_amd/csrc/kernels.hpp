@@ -92,6 +92,12 @@ struct AttnArgs {
   void* out; long o_row, o_batch;
   int sq, sk, n_q, n_kv, batch;
   int causal;
+  // optional scratch (bidirectional bf16, head_dim <= 80): when the query blocks fill the GPU's
+  // workgroup slots badly, the keys are cut into up to 3 ranges whose normalised partial outputs
+  // (bf16) and (max, sum) land here, and a second pass merges them
+  void* part = nullptr; size_t part_bytes = 0;
+  int cus = 0;                // compute units of the stream (0: all 256)
+  int kv_parts = 1;           // set by the launcher
 };
 template <typename T>
 hipError_t attention(const AttnArgs& p, int head_dim, hipStream_t s);

@@ -484,6 +484,8 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
     {
       nova::AttnArgs p{qkv, 3L * H, (long)N * 3 * H, qkv + H, 3L * H, (long)N * 3 * H, vt, skp, att, H, (long)N * H,
                        N, N, heads, heads, B, 0};
+      p.part = hmlp, p.part_bytes = (size_t)M * v->ip * sizeof(T);      // the MLP hidden is free here
+      p.cus = stream_cus(s);
       CALL(NOVA_KIND_ATTN, s, nova::attention<T>(p, hd, s));
     }
     {

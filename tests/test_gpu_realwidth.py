@@ -4,7 +4,8 @@ one by one (through the C ABI, bf16, tolerance 2e-2):
 * vision encode: one 1280-wide layer (16 heads of 80, MLP 5120) on two 1008x1008 images
   (5184 patches each) with the 2x2 merge to 3584 -- sampled merged tokens of both images; and a
   2-layer encoder with the same head size over 200 patches (a ragged last key tile) and over 288
-  and 300 patches (a last query block of 32 and 44 queries) -- every merged token;
+  and 300 patches (a last query block of 32 and 44 queries), and over 1596 patches (keys cut into
+  3 ranges merged by a second pass) -- every merged token;
 * prefill: one 3584-wide GQA layer (28/4 heads of 128, SwiGLU 18944, vocab 152064) over
   1300 visual embeddings + 200 text tokens, and over a screenshot's 3354 + 225 -- last-row logits,
   greedy id, sampled K/V;
@@ -51,9 +52,14 @@ VIT_D80 = synth.VitConfig(hidden=640, heads=8, mlp=1280, layers=2, patch=14, mer
 # per wave, halves merged at the end): with the second query group empty, and half filled.
 VIT_D80_LIGHT32 = dataclasses.replace(VIT_D80, image_h=224, image_w=252, name="vit2_d80_light32")
 VIT_D80_LIGHT44 = dataclasses.replace(VIT_D80, image_h=140, image_w=420, name="vit2_d80_light44")
+# A 38x42 grid (1596 patches) on 2 images: 7 query blocks x 8 heads x 2 images = 112 workgroups
+# fill a fifth of the GPU's slots, so the keys are cut into 3 ranges (9, 9 and 7 tiles of 64, the
+# last one ragged: 1596 = 24 x 64 + 60) merged by a second pass; the last query block (60
+# queries) is a light block.  The MLP hidden, which holds the ranges' partial rows, is 4x wide.
+VIT_D80_KEYRANGES = dataclasses.replace(VIT_D80, mlp=2560, image_h=532, image_w=588, name="vit2_d80_keyranges")
 
 
-@pytest.mark.parametrize("cfg", [VIT_D80, VIT_D80_LIGHT32, VIT_D80_LIGHT44], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [VIT_D80, VIT_D80_LIGHT32, VIT_D80_LIGHT44, VIT_D80_KEYRANGES], ids=lambda c: c.name)
 def test_vit_head80_ragged_keys(gpu_lib, cfg):
     import torch
     nova = gpu_lib
