@@ -81,7 +81,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x4 (&a
           for (int q = lane; q < TN2 * 16 * CH; q += 64) {
             const int cc = q / CH, m = row0 + (q % CH) * 8;     // 8 tokens, never across images
             if (m < p.M) {
-              const int b = m / p.vt_tokens, t = m - b * p.vt_tokens;
+              const int mg = m + p.vt_row0, b = mg / p.vt_tokens, t = mg - b * p.vt_tokens;
               const int c = col0 + jh * 16 + cc - p.v_col0, h = c / p.vt_hd, d = c - h * p.vt_hd;
               *reinterpret_cast<u32x4*>(vt + ((size_t)(b * heads + h) * p.vt_hd + d) * p.vt_pad + t) =
                   *reinterpret_cast<const u32x4*>(tl + cc * TP + (q % CH) * 8);
@@ -94,7 +94,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x4 (&a
         for (int i = 0; i < TM; ++i) {
           const int m = row0 + i * 16 + er;
           if (m >= p.M) continue;
-          const int b = m / p.vt_tokens, t = m - b * p.vt_tokens;
+          const int mg = m + p.vt_row0, b = mg / p.vt_tokens, t = mg - b * p.vt_tokens;
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int n = col0 + j * 16 + ec, c = n - p.v_col0;
@@ -621,10 +621,44 @@ static void* out_at(const GemmArgs& p, size_t rows, size_t cols) {
     return reinterpret_cast<OT*>(p.out) + rows * p.ldo + cols;
 }
 
+// Rows to run as 256x256 tiles ahead of the rest, which then run as 128x128 tiles (0: no split).
+// With many row tiles and a last round of 256x256 tiles (one workgroup per CU) that leaves much of
+// the GPU idle, the rows of whole rounds go first and the leftover rows second.  Cost in rounds of
+// 256x256 tiles: leftover 128x128 tiles that fit one workgroup per CU take about half a round,
+// each round of two per CU about 0.7; the split must save 0.3 of a round (the second launch's
+// ramp).  The screenshot encode (53 row tiles): QKV 4 -> 3.5 rounds, MLP up 5 -> 4.5, O and down
+// 2 -> 1.5; one 1008x1008 image's QKV (21 x 15 tiles): 2 -> 1.5; the 8-image MLP down (162 x 5):
+// 4 -> 3.5.
+static int row_split_rows(const GemmArgs& p) {
+  const int nm = (p.M + 255) / 256, nn = p.N / 256;
+  if (p.N % 256 || nm <= 16) return 0;
+  const long tiles = (long)nm * nn, full = tiles / 256;
+  if (full < 1) return 0;
+  const int m1 = (int)(full * 256 / nn);
+  if (m1 < 1 || m1 >= nm) return 0;
+  const long rem = (long)((p.M - m1 * 256 + 127) / 128) * (p.N / 128);
+  const double split = (double)(((long)m1 * nn + 255) / 256) + (rem <= 256 ? 0.5 : 0.71 * (double)((rem + 511) / 512));
+  return split <= (double)((tiles + 255) / 256) - 0.3 ? m1 * 256 : 0;
+}
+
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   if constexpr (sizeof(TA) == 2) {
     if (p.small_tiles) return launch_dma<OT, EPI, 128, 128, 64, 64>(p, s);
+    if constexpr (EPI != EPI_POS) {
+      if (const int m1 = row_split_rows(p)) {
+        GemmArgs a = p;
+        a.M = m1;
+        hipError_t e = launch_dma<OT, EPI, 256, 256, 64, 128>(a, s);
+        if (e != hipSuccess) return e;
+        GemmArgs b = p;
+        b.M = p.M - m1;
+        b.A = reinterpret_cast<const bf16_t*>(p.A) + (size_t)m1 * p.lda;
+        b.out = out_at<OT, EPI>(p, m1, 0);
+        b.vt_row0 = p.vt_row0 + m1;
+        return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
+      }
+    }
   }
   // 256x256 tiles with 8 waves (two per SIMD, each 64x128) when there are at least two tiles per
   // CU; otherwise 128x128 tiles with 4 waves (two workgroups per CU), with K split into slices
@@ -666,7 +700,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
     }
     // 256x256 tiles that fill at least three quarters of one round of the GPU (one workgroup per
     // CU) beat two rounds of 128x128 tiles (the 3.6k-token prefill's QKV projection: 14 x 18
-    // tiles, 157 -> 99 us; the one-image encode's QKV and MLP up projections)
+    // tiles, 157 -> 99 us; the one-image encode's MLP up projection)
     if (p.N % 256 == 0 && tiles256 >= 192 && tiles256 < 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     if (!(p.N % 256 == 0 && tiles256 >= 512) && p.vt == nullptr) {
       const int sl = split_slices(p);
@@ -705,22 +739,6 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         b.W = p.W + (size_t)n1 * p.ldw;
         if (p.bias) b.bias = p.bias + n1;
         b.out = out_at<OT, EPI>(p, 0, EPI == EPI_SWIGLU ? n1 / 2 : n1);
-        return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
-      }
-      // many row tiles and a long K with a last round of 256x256 tiles mostly idle (the ViT's MLP
-      // down projection at 8 images: 810 tiles, K = 5120): the rows of whole rounds as 256x256
-      // tiles, the remaining rows as 128x128 tiles, which fit the GPU in one round
-      const int m_tiles1 = (int)(rounds * 256 / (p.N / 256));
-      if (p.K >= 4096 && tiles % 256 != 0 && tiles % 256 < 64 && m_tiles1 > 16 && m_tiles1 < nm && EPI != EPI_POS &&
-          p.vt == nullptr) {
-        GemmArgs a = p;
-        a.M = m_tiles1 * 256;
-        hipError_t e = launch_dma<OT, EPI, 256, 256, 64, 128>(a, s);
-        if (e != hipSuccess) return e;
-        GemmArgs b = p;
-        b.M = p.M - a.M;
-        b.A = reinterpret_cast<const bf16_t*>(p.A) + (size_t)a.M * p.lda;
-        b.out = out_at<OT, EPI>(p, a.M, 0);
         return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
       }
       return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);

@@ -34,6 +34,7 @@ struct GemmArgs {
   // lands at vt[((b * heads + h) * vt_hd + d) * vt_pad + t].  Requires v_col0 % 256 == 0,
   // vt_tokens % 8 == 0 and vt_pad % 8 == 0 (checked by the caller).
   void* vt = nullptr; int v_col0 = 0, vt_hd = 0, vt_tokens = 0, vt_pad = 0;
+  int vt_row0 = 0;            // set by the launcher: row m of this launch is row vt_row0 + m above
   // bf16 only: always 128x128 tiles of 4 waves, unsplit (a kernel that leaves room on every CU for
   // another kernel's workgroups: the intra-CU co-residency variant)
   bool small_tiles = false;

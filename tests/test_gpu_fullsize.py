@@ -2,9 +2,11 @@
 that hold at any size (the oracle would need minutes per image or sequence at full depth; the
 real-width single-layer tests hold the kernels to the oracle at these shapes):
 
-* vision encode, ViT-32 (1280 wide, 32 layers) on 8 images of 1008x1008 in one batch: each
-  image's output equals its output when encoded alone (rows never mix, so the equality is exact),
-  a second pass repeats the first bit for bit, and every value is finite;
+* vision encode, ViT-32 (1280 wide, 32 layers) on 8 images of 1008x1008 in one batch: a second
+  pass repeats the first bit for bit, every value is finite, and each image's output matches its
+  output when encoded alone -- rows never mix, but the one-image pass is a different bf16 path: its
+  attention cuts the keys into 3 ranges merged from bf16 partial rows (one image's query blocks
+  fill a third of the workgroup slots less), so the two agree within the two-path depth bound;
 * prefill of 1300 visual + 200 text tokens through the 28-layer 3584-wide LLM, against a
   prefill of the first 1499 tokens followed by one decode step on the 1500th: the same last-row
   logits through other kernels (GEMM and tiled attention against thin GEMM and paged decode
@@ -17,7 +19,7 @@ Tolerance between two bf16 paths at full depth: at one layer both sit within the
 oracle; the two paths round in different orders at every layer, and independent per-layer
 rounding grows like the square root of the depth, so the bound is 2e-2 * sqrt(L) (measured: 0.8%
 at one layer, 1.8% at 8, 3.7% at 28 for prefill against prefix + decode).  Computations that are
-the same row by row (a prefix of the prompt, an image within a batch) must agree exactly.
+the same row by row (a prefix of the prompt) must agree exactly.
 """
 import math
 
@@ -49,7 +51,9 @@ def test_encode_bench_config_batch_invariant(gpu_lib):
     assert torch.equal(out, again)
     for i in (0, 5, 7):
         alone = vit.encode(px[i:i + 1].contiguous())
-        assert torch.equal(alone[0], out[i]), f"image {i}"
+        err = vlm.max_rel_err(alone[0].float().cpu().numpy(), out[i].float().cpu().numpy())
+        print(f"image {i} alone vs in the batch: max rel err {err:.2e}")
+        assert err < depth_tol(cfg.layers), f"image {i}: {err}"
 
 
 @pytest.fixture(scope="module")
