@@ -87,3 +87,29 @@ def test_ragged_prefill_and_batched_decode(gpu_lib, ref, mode):
             assert np.array_equal(nx, nx_ref), f"step {t}"
     ek, ev = sc.kv_errors(ref["kv"].k, ref["kv"].v, kv.k5.float().cpu().numpy(), kv.v5.float().cpu().numpy())
     assert ek < tol and ev < tol
+
+
+def test_long_prefill_every_position(gpu_lib):
+    """A 700-token bf16 prefill (600 visual + 100 text) on the tiny LLM: six causal query blocks
+    of 128 (2 .. 11 key tiles of 64, the last block ragged).  Last-row logits and the K/V of both
+    layers at every position (layer 1's K/V come from layer 0's attention output of every row)
+    against the oracle."""
+    import torch
+    nova = gpu_lib
+    cfg = synth.TINY_LLM
+    w = synth.llm_weights(cfg, 0)
+    nv, nt = 600, 100
+    vis = synth.vision_embeds(nv, cfg.hidden, seed=31)
+    ids = synth.text_ids(nt, cfg.vocab, seed=32)
+    tables, pool = synth.block_tables([nv + nt], cfg.block, seed=33)
+    kv_ref = vlm.PagedKV(cfg.layers, pool, cfg.n_kv, cfg.block, cfg.head_dim)
+    lg_ref, _ = vlm.llm_prefill(vis, ids, w, cfg, kv=kv_ref, table=tables[0])
+    llm = nova.Llm(cfg, w, act=nova.ACT_BF16)
+    kv = nova.KvPool(llm, pool)
+    lg = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+    llm.prefill(torch.from_numpy(vis).to("cuda", torch.bfloat16), torch.from_numpy(ids).to("cuda"),
+                torch.from_numpy(tables[0]).to("cuda"), kv, logits=lg)
+    torch.cuda.synchronize()
+    assert vlm.max_rel_err(lg.cpu().numpy(), lg_ref) < sc.TOL_BF16
+    ek, ev = sc.kv_errors(kv_ref.k, kv_ref.v, kv.k5.float().cpu().numpy(), kv.v5.float().cpu().numpy())
+    assert ek < sc.TOL_BF16 and ev < sc.TOL_BF16, (ek, ev)
