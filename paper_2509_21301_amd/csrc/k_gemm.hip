@@ -671,11 +671,12 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
     // without the split partials' traffic
     if (p.N % 256 == 0 && p.K >= 8192 && tiles256 >= 192 && tiles256 <= 256)
       return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
-    // a very long K whose 256x256 tiles fill under three quarters of the GPU (the 1500-token
-    // prefill's down projection: 6 x 14 tiles, K = 18944): K slices of 256x256 tiles that make one
-    // round of at least 224 of the 256 CUs (3 slices of 6336, 6336 and 6272 there), then the
-    // fp32 partials summed in slice order
-    if (p.split_ws && p.vt == nullptr && p.N % 256 == 0 && p.K >= 8192 && tiles256 < 192) {
+    // a long K whose 256x256 tiles fill under three quarters of the GPU (the 1500-token prefill's
+    // down projection: 6 x 14 tiles, K = 18944; its O projection: 6 x 14 tiles, K = 3584): K
+    // slices of 256x256 tiles that make one round of at least 224 of the 256 CUs (3 slices of
+    // 6336, 6336 and 6272, and of 1216, 1216 and 1152 there), then the fp32 partials summed in
+    // slice order
+    if (p.split_ws && p.vt == nullptr && p.N % 256 == 0 && p.K >= 3072 && tiles256 < 192) {
       int sl = 0;
       for (int c = 2; c <= 4 && !sl; ++c) {
         const int kslice = (p.K / BK + c - 1) / c * BK;
