@@ -120,73 +120,86 @@ hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* 
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ rotary embedding in place
-// Half-split pairing: (c, c + D/2) rotate by angle pos * theta^(-2c/D).  A thread takes one
-// 16-byte piece of each half (8 bf16 or 4 fp32 pairs); the inverse frequencies are computed once
-// per workgroup, and each angle is formed and reduced in double before the fp32 sine/cosine, as
-// in the decode kernel.
+// ------------------------------------------------------------------ projected rows -> attention inputs
+// One pass over the packed QKV rows of a prefill (or a bidirectional encode): workgroup (64-token
+// tile, head, batch) of a grid over every q, k and v head.
+//  * q and k heads (rope_theta > 0): rotary embedding in place, half-split pairing (c, c + D/2)
+//    by angle pos * theta^(-2c/D); a thread takes one 16-byte piece of each half (8 bf16 or 4 fp32
+//    pairs); the inverse frequencies are computed once per workgroup and each angle is formed and
+//    reduced in double before the fp32 sine/cosine, as in the decode step's table.  A k head also
+//    appends its rotated rows to the paged cache K [blk][kvh][slot][D] (16-byte pieces).
+//  * v heads: V^T [b][kv head][D][sk_pad] for the attention kernel (keys past S zero) and the
+//    paged V [blk][kvh][D][slot], through an LDS tile: 16-byte reads of each token's D values,
+//    16-byte writes of 16 / sizeof(T) consecutive keys of each V^T row.
 template <typename T>
-__global__ void __launch_bounds__(256) rope_inplace_kernel(T* __restrict__ qkv, int rows, int S, int n_rot_heads, int D,
-                                                           float theta, int pos0, int ld) {
-  constexpr int V = 16 / sizeof(T);
-  __shared__ double inv_s[64];                       // D / 2 <= 64
-  const int half = D / 2;
-  for (int c = threadIdx.x; c < half; c += blockDim.x) inv_s[c] = exp2(-(2.0 * c / D) * log2((double)theta));
-  __syncthreads();
-  const int pieces = half / V;
-  const long total = (long)rows * n_rot_heads * pieces;
-  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
-    const int pc = (int)(idx % pieces);
-    const long t = idx / pieces;
-    const int hh = (int)(t % n_rot_heads);
-    const int row = (int)(t / n_rot_heads);
-    const double pos = (double)(pos0 + row % S);
-    T* e1 = qkv + (size_t)row * ld + (size_t)hh * D + pc * V;
-    T* e2 = e1 + half;
-    T a[V], bv[V];
-    *reinterpret_cast<u32x4*>(a) = *reinterpret_cast<const u32x4*>(e1);
-    *reinterpret_cast<u32x4*>(bv) = *reinterpret_cast<const u32x4*>(e2);
-#pragma unroll
-    for (int v = 0; v < V; ++v) {
-      double ang = pos * inv_s[pc * V + v];
-      ang -= 6.283185307179586 * floor(ang * 0.15915494309189535);
-      float sn, cs;
-      sincosf((float)ang, &sn, &cs);
-      const float x1 = to_f<T>(a[v]), x2 = to_f<T>(bv[v]);
-      a[v] = from_f<T>(x1 * cs - x2 * sn);
-      bv[v] = from_f<T>(x2 * cs + x1 * sn);
-    }
-    *reinterpret_cast<u32x4*>(e1) = *reinterpret_cast<const u32x4*>(a);
-    *reinterpret_cast<u32x4*>(e2) = *reinterpret_cast<const u32x4*>(bv);
-  }
-}
-
-// ------------------------------------------------------------------ V transpose and paged K/V append
-// V of the projected rows -> V^T [b][kv head][D][sk_pad] (keys past S zero) for the attention
-// kernel, and for a paged cache K [blk][kvh][slot][D], V [blk][kvh][D][slot].  A block moves 64
-// tokens of one kv head through an LDS tile: 16-byte reads of each token's D values, 16-byte
-// writes of 16 / sizeof(T) consecutive keys of each V^T row.
-template <typename T>
-__global__ void __launch_bounds__(256) kv_scatter_kernel(const T* __restrict__ qkv, int S, int n_q, int n_kv, int D,
-                                                        T* __restrict__ vt, int sk_pad, T* __restrict__ kpool,
-                                                        T* __restrict__ vpool, const int* __restrict__ table, int block) {
-  constexpr int EPC = 16 / sizeof(T);      // elements per 16-byte chunk
+__global__ void __launch_bounds__(256) qkv_prefill_kernel(T* __restrict__ qkv, int S, int n_q, int n_kv, int D, float theta,
+                                                          int pos0, T* __restrict__ vt, int sk_pad, T* __restrict__ kpool,
+                                                          T* __restrict__ vpool, const int* __restrict__ table, int block,
+                                                          int h0) {
+  constexpr int EPC = 16 / sizeof(T);      // elements per 16-byte piece
   constexpr int TP = 128 + EPC;            // tile pitch (elements), D <= 128
   __shared__ __align__(16) T tile[64 * TP];
-  const int t0 = blockIdx.x * 64, kvh = blockIdx.y, b = blockIdx.z;
+  __shared__ double inv_s[64];             // D / 2 <= 64
+  const int t0 = blockIdx.x * 64, hh = h0 + blockIdx.y, b = blockIdx.z;
   const int ld = (n_q + 2 * n_kv) * D;
-  const T* vsrc = qkv + (size_t)b * S * ld + (size_t)(n_q + n_kv) * D + (size_t)kvh * D;
-  const T* ksrc = qkv + (size_t)b * S * ld + (size_t)n_q * D + (size_t)kvh * D;
+  T* rows = qkv + (size_t)b * S * ld + (size_t)hh * D;
+  if (hh < n_q + n_kv) {
+    const bool khead = hh >= n_q;
+    if (theta <= 0.f) {
+      if (!khead || table == nullptr) return;
+      // no rotation: the k rows go to the cache as they are
+      for (int i = threadIdx.x; i < 64 * (D / EPC); i += 256) {
+        const int t = i / (D / EPC), c = (i % (D / EPC)) * EPC, tok = t0 + t;
+        if (tok >= S) continue;
+        const int phys = table[tok / block], slot = tok % block;
+        *reinterpret_cast<u32x4*>(kpool + (((size_t)phys * n_kv + (hh - n_q)) * block + slot) * D + c) =
+            *reinterpret_cast<const u32x4*>(rows + (size_t)tok * ld + c);
+      }
+      return;
+    }
+    const int half = D / 2, pieces = half / EPC;
+    for (int c = threadIdx.x; c < half; c += 256) inv_s[c] = exp2(-(2.0 * c / D) * log2((double)theta));
+    __syncthreads();
+    for (int i = threadIdx.x; i < 64 * pieces; i += 256) {
+      const int t = i / pieces, pc = i % pieces, tok = t0 + t;
+      if (tok >= S) continue;
+      T* e1 = rows + (size_t)tok * ld + pc * EPC;
+      T* e2 = e1 + half;
+      T a[EPC], bv[EPC];
+      *reinterpret_cast<u32x4*>(a) = *reinterpret_cast<const u32x4*>(e1);
+      *reinterpret_cast<u32x4*>(bv) = *reinterpret_cast<const u32x4*>(e2);
+      const double pos = (double)(pos0 + tok);
+#pragma unroll
+      for (int v = 0; v < EPC; ++v) {
+        double ang = pos * inv_s[pc * EPC + v];
+        ang -= 6.283185307179586 * floor(ang * 0.15915494309189535);
+        float sn, cs;
+        sincosf((float)ang, &sn, &cs);
+        const float x1 = to_f<T>(a[v]), x2 = to_f<T>(bv[v]);
+        a[v] = from_f<T>(x1 * cs - x2 * sn);
+        bv[v] = from_f<T>(x2 * cs + x1 * sn);
+      }
+      *reinterpret_cast<u32x4*>(e1) = *reinterpret_cast<const u32x4*>(a);
+      *reinterpret_cast<u32x4*>(e2) = *reinterpret_cast<const u32x4*>(bv);
+      if (khead && table != nullptr) {
+        T* kd = kpool + (((size_t)table[tok / block] * n_kv + (hh - n_q)) * block + tok % block) * D + pc * EPC;
+        *reinterpret_cast<u32x4*>(kd) = *reinterpret_cast<const u32x4*>(a);
+        *reinterpret_cast<u32x4*>(kd + half) = *reinterpret_cast<const u32x4*>(bv);
+      }
+    }
+    return;
+  }
+  const int kvh = hh - n_q - n_kv;
   const int cpr = D / EPC;
   for (int c = threadIdx.x; c < 64 * cpr; c += 256) {
     const int t = c / cpr, d0 = (c % cpr) * EPC;
     u32x4 val = {0u, 0u, 0u, 0u};
-    if (t0 + t < S) val = *reinterpret_cast<const u32x4*>(vsrc + (size_t)(t0 + t) * ld + d0);
+    if (t0 + t < S) val = *reinterpret_cast<const u32x4*>(rows + (size_t)(t0 + t) * ld + d0);
     *reinterpret_cast<u32x4*>(tile + t * TP + d0) = val;
   }
   __syncthreads();
   T* vdst = vt + ((size_t)b * n_kv + kvh) * D * (size_t)sk_pad;
-  constexpr int TCN = 64 / EPC;            // key chunks per V^T row of this block
+  constexpr int TCN = 64 / EPC;            // key pieces per V^T row of this tile
   for (int c = threadIdx.x; c < D * TCN; c += 256) {
     const int d = c / TCN, tc = (c % TCN) * EPC;
     T vals[EPC];
@@ -205,17 +218,6 @@ __global__ void __launch_bounds__(256) kv_scatter_kernel(const T* __restrict__ q
       }
     }
   }
-  if (table == nullptr) return;
-  // K rows: D contiguous elements in both layouts, copied 16 bytes at a time
-  const int kc = D / EPC;
-  for (int i = threadIdx.x; i < 64 * kc; i += 256) {
-    const int t = i / kc, c = (i % kc) * EPC;
-    const int tok = t0 + t;
-    if (tok >= S) continue;
-    const int phys = table[tok / block], slot = tok % block;
-    *reinterpret_cast<u32x4*>(kpool + (((size_t)phys * n_kv + kvh) * block + slot) * D + c) =
-        *reinterpret_cast<const u32x4*>(ksrc + (size_t)tok * ld + c);
-  }
 }
 
 template <typename T>
@@ -223,18 +225,12 @@ hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float
                        int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s) {
   if (S <= 0) return hipSuccess;
   if (D > 128 || D % 16 || sk_pad < S || sk_pad % 64) return hipErrorInvalidValue;
-  const int ld = (n_q + 2 * n_kv) * D;
-  if (rope_theta > 0.f) {
-    const long total = (long)batch * S * (n_q + n_kv) * (D / 2 / (16 / (int)sizeof(T)));
-    const int grid = (int)std::min<long>((total + 255) / 256, 65536);
-    hipLaunchKernelGGL((rope_inplace_kernel<T>), dim3(grid), dim3(256), 0, s, qkv, batch * S, S, n_q + n_kv, D,
-                       rope_theta, pos0, ld);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  dim3 grid(sk_pad / 64, n_kv, batch);
-  hipLaunchKernelGGL((kv_scatter_kernel<T>), grid, dim3(256), 0, s, qkv, S, n_q, n_kv, D, vt, sk_pad, kpool, vpool,
-                     table, block);
+  if (table != nullptr && block % (16 / (int)sizeof(T))) return hipErrorInvalidValue;
+  // with no rotation and no cache, only the v heads have work
+  const int h0 = rope_theta > 0.f || table != nullptr ? 0 : n_q + n_kv;
+  dim3 grid(sk_pad / 64, n_q + 2 * n_kv - h0, batch);
+  hipLaunchKernelGGL((qkv_prefill_kernel<T>), grid, dim3(256), 0, s, qkv, S, n_q, n_kv, D, rope_theta, pos0, vt, sk_pad,
+                     kpool, vpool, table, block, h0);
   return hipGetLastError();
 }
 
