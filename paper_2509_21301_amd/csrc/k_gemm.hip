@@ -18,6 +18,15 @@
 
 namespace nova {
 
+// The dispatcher deals workgroup b of a launch to XCD b % 8.  Renumbered so that each XCD takes
+// one contiguous range of the n tile ids (the first n % 8 XCDs one more than the others), the
+// tiles resident on an XCD at a time are neighbours and share A and W panels in its L2, whatever
+// n is (with an 8-way round-robin of plain ids, no two neighbouring tiles share an L2).
+__device__ __forceinline__ int xcd_contiguous(int b, int n) {
+  const int q = n >> 3, r = n & 7, x = b & 7, j = b >> 3;
+  return x < r ? x * (q + 1) + j : r * (q + 1) + (x - r) * q + j;
+}
+
 constexpr int BK = 64;
 constexpr int PAD = 8;             // bf16 elements of row padding in LDS
 constexpr int LDK = BK + PAD;      // LDS row pitch (elements)
@@ -198,8 +207,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_kernel(GemmAr
   // ---- tile index: XCD-contiguous, then grouped along M for L2 reuse of W
   const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
   const int total = nm * nn;
-  int id = blockIdx.x;
-  if ((total & 7) == 0) id = (id & 7) * (total >> 3) + (id >> 3);
+  const int id = xcd_contiguous(blockIdx.x, gridDim.x);
   constexpr int G = 8;
   const int group = id / (G * nn);
   const int first_m = group * G;
@@ -347,12 +355,16 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64) gemm_dma_kernel(Ge
   const int nm = (p.M + BM - 1) / BM, nn = p.N / BN;
   const int total = nm * nn;
   // split K: workgroup blockIdx.x / total takes K slice number that many, writing fp32 partials
-  const int ks = p.kslice ? blockIdx.x / total : 0;
-  int id = blockIdx.x - ks * total;
-  if ((total & 7) == 0) id = (id & 7) * (total >> 3) + (id >> 3);
+  const int idg = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int ks = p.kslice ? idg / total : 0;
+  const int id = idg - ks * total;
   // groups of G M-tiles sweep the N tiles together (an XCD's ~32 resident tiles then share a few
-  // A and W panels in its L2); measured best at 16 for 256-row tiles and 8 for 128-row tiles
-  constexpr int G = BM >= 256 ? 16 : 8;
+  // A and W panels in its L2): 256-row tiles in groups of 4 when there are many row tiles (the
+  // XCD's A panels stay in its L2 while the group sweeps N: encode GEMM family 53.1 -> 50.7 ms
+  // per pass against groups of 16, one-image encode 14.04 -> 13.87 ms), of 16 (all of them) when
+  // there are at most 16 (the 1500-token prefill: 20.30 -> 20.03 ms against groups of 4); 8 for
+  // 128-row tiles
+  const int G = BM >= 256 ? (nm <= 16 ? 16 : 4) : 8;
   const int group = id / (G * nn);
   const int first_m = group * G;
   const int gsize = min(nm - first_m, G);
