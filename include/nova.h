@@ -192,7 +192,9 @@ int nova_llm_prefill(const nova_llm* llm, const void* vis, int n_vis, const int3
 /* One in-flight-batched decode step for `batch` sequences (batch <= 32).
  *  ids, pos:     device int32 [batch]: token fed and its position (context becomes pos + 1)
  *  block_tables: device int32 [batch, max_blocks] (row b covers positions 0..pos[b])
- *  max_ctx:      an upper bound of pos[b] + 1 over the batch (sizes the attention split)
+ *  max_ctx:      an upper bound of pos[b] + 1 over the batch (sizes the attention split); a
+ *                position outside 0..max_ctx - 1 is clamped into it (garbage out, no access
+ *                outside the sequence's block-table row)
  *  Appends each sequence's K/V at pos[b], writes next_ids (device int32 [batch]) and, if
  *  logits != NULL, device fp32 [batch, vocab]. */
 int nova_llm_decode(const nova_llm* llm, const int32_t* ids, const int32_t* pos, const int32_t* block_tables,

@@ -62,7 +62,9 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) d
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int G = p.n_q / p.n_kv;
   const int col = lane & 15, grp = lane >> 4;
-  const int ps = p.pos[b];
+  // a position past the documented bound (pos + 1 <= max_ctx, which the block-table width covers)
+  // is clamped, so no table or cache access leaves the sequence's row whatever the caller passes
+  const int ps = min(max(p.pos[b], 0), p.max_ctx - 1);
   const int ctx = ps + 1;
   const int nblk = (ctx + DA_BLOCK - 1) / DA_BLOCK;
   const int pair_begin = split * pairs_per_split;
