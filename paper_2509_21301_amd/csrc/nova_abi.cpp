@@ -47,6 +47,8 @@ struct Global {
   int cus = 0;
   std::mutex mu;
   std::map<std::vector<uint32_t>, hipStream_t> mask_streams;   // partition stream pool
+  std::map<std::vector<uint32_t>, uint64_t> mask_used;          // its last use (a counter)
+  uint64_t uses = 0;
   hipStream_t full_streams[3] = {nullptr, nullptr, nullptr};   // whole-GPU mask, one per stage
   hipStream_t stage_stream[3] = {nullptr, nullptr, nullptr};
   hipEvent_t stage_switch[3] = {nullptr, nullptr, nullptr};
@@ -134,6 +136,7 @@ extern "C" int nova_init(int device) {
 extern "C" void nova_shutdown(void) {
   std::lock_guard<std::mutex> lk(g.mu);
   for (auto& kv : g.mask_streams) hipStreamDestroy(kv.second);
+  g.mask_used.clear();
   for (auto& fs : g.full_streams) {
     if (fs) hipStreamDestroy(fs);
     fs = nullptr;
@@ -983,6 +986,38 @@ extern "C" int nova_make_cu_mask(int n_cus, int first_slot, uint32_t* mask) {
   return NOVA_OK;
 }
 
+namespace {
+// Each CU-masked stream holds a hardware queue of its own, and past about a dozen of them in one
+// process every queue's work slows down, idle ones included (measured: the whole-GPU 8-image encode
+// on another stream 89 ms with 12 masked streams alive, 156 ms with 24, 705 ms with 140).  The pool
+// therefore keeps at most this many; before it grows past that, the least recently used streams
+// that no stage holds are drained and destroyed (a caller keeps a stage's stream until its next
+// partition call for that stage, which is never evicted).
+constexpr size_t kMaxMaskStreams = 8;
+
+void make_room_for_mask_streams(const std::vector<uint32_t>& keep) {
+  std::vector<uint32_t> comp(8);
+  for (int w = 0; w < 8; ++w) comp[w] = ~keep[w];
+  while (g.mask_streams.size() + 2 > kMaxMaskStreams) {
+    const std::vector<uint32_t>* victim = nullptr;
+    uint64_t oldest = ~0ull;
+    for (auto& kv : g.mask_streams) {
+      bool held = kv.first == keep || kv.first == comp;
+      for (int st = 0; st < 3 && !held; ++st) held = g.stage_stream[st] == kv.second;
+      const uint64_t u = g.mask_used[kv.first];
+      if (!held && u < oldest) { oldest = u; victim = &kv.first; }
+    }
+    if (!victim) return;                  // every pooled stream is held: grow past the cap
+    const std::vector<uint32_t> v = *victim;
+    hipStream_t s = g.mask_streams[v];
+    hipStreamSynchronize(s);
+    hipStreamDestroy(s);
+    g.mask_streams.erase(v);
+    g.mask_used.erase(v);
+  }
+}
+}  // namespace
+
 extern "C" int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int mask_words, nova_stream_t* out_stream) {
   if (stage < 0 || stage > 2) return fail(NOVA_EINVAL, "stage %d out of range", stage);
   if (!cu_mask || !out_stream || mask_words <= 0 || mask_words > 8) return fail(NOVA_EINVAL, "mask needs 1..8 words");
@@ -1012,6 +1047,7 @@ extern "C" int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int 
     }
     ns = g.full_streams[stage];
   } else if (g.mask_streams.find(m) == g.mask_streams.end()) {
+    make_room_for_mask_streams(m);
     hipError_t e = hipExtStreamCreateWithCUMask(&ns, 8, m.data());
     if (e != hipSuccess) return fail(NOVA_EHIP, "hipExtStreamCreateWithCUMask: %s", hipGetErrorString(e));
     g.mask_streams[m] = ns;
@@ -1033,10 +1069,12 @@ extern "C" int nova_set_stage_partition(int stage, const uint32_t* cu_mask, int 
       e = hipExtStreamCreateWithCUMask(&cs, 8, c.data());
       if (e != hipSuccess) return fail(NOVA_EHIP, "hipExtStreamCreateWithCUMask: %s", hipGetErrorString(e));
       g.mask_streams[c] = cs;
+      g.mask_used[c] = ++g.uses;
     }
   } else {
     ns = g.mask_streams[m];
   }
+  if (!full) g.mask_used[m] = ++g.uses;
   hipStream_t old = g.stage_stream[stage];
   if (old && old != ns) {
     if (!g.stage_switch[stage]) HIP_TRY(hipEventCreateWithFlags(&g.stage_switch[stage], hipEventDisableTiming));
