@@ -141,6 +141,24 @@ def time_passes(torch, fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
+def time_each(torch, fn, reps, stream):
+    """Per-pass times (ms), each pass between its own pair of HIP events on the stream."""
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record(stream)
+    for i in range(reps):
+        fn()
+        ev[i + 1].record(stream)
+    ev[-1].synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]
+
+
+def spread(ts):
+    """Median, 10th and 90th percentile of pass times (ms)."""
+    q = np.percentile(np.asarray(ts), [50, 10, 90])
+    return {"ms": round(float(q[0]), 3), "ms_p10": round(float(q[1]), 3), "ms_p90": round(float(q[2]), 3)}
+
+
 class Stages:
     """The three stage workloads on one GPU, each callable on a given stream."""
 
@@ -751,24 +769,31 @@ def main():
         print(json.dumps(result), flush=True)
         return
 
-    # ---------------- per-stage throughput on all CUs
+    # ---------------- per-stage throughput on all CUs: median (p10, p90) of per-pass event times,
+    # rates and roofline fractions at the median (useful flops only; decode against HBM bytes)
     stages = {}
     for b in (1, 4, 8):
         if b > B:
             continue
-        t = time_passes(torch, lambda: st.encode(b), 3, stream)
-        stages[f"encode_b{b}"] = {"ms": round(t, 3), "patches_per_s": round(b * vc.n_patches / (t / 1e3), 1),
-                                  "tflops": round(sum(vit_flops(vc, b)) / (t / 1e3) / 1e12, 1)}
+        st.encode(b)
+        sp = spread(time_each(torch, lambda: st.encode(b), 10, stream))
+        t = sp["ms"]
+        tf = sum(vit_flops(vc, b)) / (t / 1e3) / 1e12
+        stages[f"encode_b{b}"] = {**sp, "patches_per_s": round(b * vc.n_patches / (t / 1e3), 1),
+                                  "tflops": round(tf, 1), "frac": round(tf / BF16_PEAK_TFLOPS, 3)}
     st.prefill()
-    t = time_passes(torch, st.prefill, 5, stream)
+    sp = spread(time_each(torch, st.prefill, 20, stream))
+    t = sp["ms"]
     pf_lin, pf_attn = prefill_flops(lc, st.s)
-    stages["prefill_s1500"] = {"ms": round(t, 3), "tok_per_s": round(st.s / (t / 1e3), 1),
-                               "tflops": round((pf_lin + pf_attn) / (t / 1e3) / 1e12, 1)}
+    tf = (pf_lin + pf_attn) / (t / 1e3) / 1e12
+    stages["prefill_s1500"] = {**sp, "tok_per_s": round(st.s / (t / 1e3), 1), "tflops": round(tf, 1),
+                               "frac": round(tf / BF16_PEAK_TFLOPS, 3)}
     for b in (1, 8, 32):
         st.decode(b)
-        t = time_passes(torch, lambda: st.decode(b), 10, stream)
+        sp = spread(time_each(torch, lambda: st.decode(b), 30, stream))
+        t = sp["ms"]
         wb, kvb = decode_bytes(lc, b, st.s + 1)          # every sequence sits at position s: s + 1 keys
-        stages[f"decode_b{b}"] = {"ms": round(t, 3), "tok_per_s": round(b / (t / 1e3), 1),
+        stages[f"decode_b{b}"] = {**sp, "tok_per_s": round(b / (t / 1e3), 1),
                                   "hbm_gbs": round((wb + kvb) / (t / 1e3) / 1e9, 1),
                                   "hbm_frac": round((wb + kvb) / (t / 1e3) / 1e9 / HBM_PEAK_GBS, 3)}
     result["stages"] = stages
@@ -777,7 +802,14 @@ def main():
     # ---------------- CU-share curves and co-run (XCD-balanced partitions)
     if not args.no_sweep:
         shares = [32, 64, 96, 128, 160, 192, 224, 256]
-        curves = {"shares": shares, "encode_b1_patches_per_s": [], "prefill_tok_per_s": [], "decode_b8_tok_per_s": []}
+        curves = {"shares": shares, "encode_b1_patches_per_s": [], "prefill_tok_per_s": [], "decode_b8_tok_per_s": [],
+                  # fractions of the full-GPU peak and of the share's own compute peak (P / 256 of it);
+                  # decode against the full HBM bandwidth
+                  "encode_b1_frac": [], "encode_b1_frac_of_share": [], "prefill_frac": [], "prefill_frac_of_share": [],
+                  "decode_b8_hbm_frac": []}
+        enc1_flops = sum(vit_flops(vc, 1))
+        pf_flops = sum(prefill_flops(lc, st.s))
+        dec8_bytes = sum(decode_bytes(lc, 8, st.s + 1))
         for p in shares:
             ms_e = ms_p = ms_d = None
             s_e = nova.set_stage_partition(nova.STAGE_ENCODE, nova.make_cu_mask(p, 0))
@@ -789,6 +821,13 @@ def main():
             curves["encode_b1_patches_per_s"].append(round(vc.n_patches / (ms_e / 1e3), 1))
             curves["prefill_tok_per_s"].append(round(st.s / (ms_p / 1e3), 1))
             curves["decode_b8_tok_per_s"].append(round(8 / (ms_d / 1e3), 1))
+            fe = enc1_flops / (ms_e / 1e3) / 1e12 / BF16_PEAK_TFLOPS
+            fp = pf_flops / (ms_p / 1e3) / 1e12 / BF16_PEAK_TFLOPS
+            curves["encode_b1_frac"].append(round(fe, 3))
+            curves["encode_b1_frac_of_share"].append(round(fe * 256 / p, 3))
+            curves["prefill_frac"].append(round(fp, 3))
+            curves["prefill_frac_of_share"].append(round(fp * 256 / p, 3))
+            curves["decode_b8_hbm_frac"].append(round(dec8_bytes / (ms_d / 1e3) / 1e9 / HBM_PEAK_GBS, 3))
             log(f"share {p:3d} CUs: encode {ms_e:.2f} ms, prefill {ms_p:.2f} ms, decode(b8) {ms_d:.3f} ms")
         result["cu_share_curves"] = curves
         # co-run on the serving shapes: decode (batch 8) on P CUs with the screenshot encode or a
