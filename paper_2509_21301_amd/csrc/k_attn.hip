@@ -62,7 +62,12 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_kernel(AttnArgs p) {
   {
     const int pairs = p.batch * p.n_q, lin = blockIdx.x;
     int pair;
-    if (pairs % 8 == 0) {
+    if (CAUSAL) {
+      // heaviest blocks of every head first: the workgroups dispatched last, which share a CU
+      // with an earlier one, are the lightest; head h's blocks fall on XCDs (h + pairs k) % 8
+      qbi = lin / pairs;
+      pair = lin % pairs;
+    } else if (pairs % 8 == 0) {
       const int j = lin >> 3;
       pair = (lin & 7) * (pairs >> 3) + j / nqb;
       qbi = j % nqb;
