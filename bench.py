@@ -256,20 +256,27 @@ class ServingSetup:
 
 
 # ----------------------------------------------------------------------------- serving runs
-def serving_modes(sched, curves, out_len, rate, adaptive):
+def serving_modes(sched, curves, out_len, rate, adaptive, adaptive32=None):
     """The systems compared on one trace: Nova at the rate's Pareto point (Eq. 1 + Eq. 6) and with
     the Eq. 5 adaptation (parameters from adaptive_params), time slicing decode-first and
     prefill-first, the PF-Limit baseline (prefill-first, decode once more than 5 wait; Sec. 5.1),
     and unpartitioned streams (Multi-Stream)."""
     rv, rp, _ = sched.best_under_load(sched.on_granule(curves), out_len, rate)
     a = adaptive
-    return [("nova_rate_static", dict(mode="nova", decode_cus=(rv, rp))),
-            ("nova_adaptive", dict(mode="nova", decode_cus=(a["sm_op_v"], a["sm_op_p"]),
-                                   alpha=(a["alpha_v"], a["alpha_p"]), minimum=a["sm_min"])),
-            ("time_sliced_decode_first", dict(mode="time_sliced", slice_order="decode_first")),
-            ("time_sliced_prefill_first", dict(mode="time_sliced", slice_order="prefill_first")),
-            ("pf_limit", dict(mode="time_sliced", slice_order="prefill_first", decode_limit=5)),
-            ("multi_stream", dict(mode="multi_stream"))]
+    modes = [("nova_rate_static", dict(mode="nova", decode_cus=(rv, rp))),
+             ("nova_adaptive", dict(mode="nova", decode_cus=(a["sm_op_v"], a["sm_op_p"]),
+                                    alpha=(a["alpha_v"], a["alpha_p"]), minimum=a["sm_min"]))]
+    if adaptive32 is not None:
+        # the same adaptation on shares of whole mask words (32 CUs): at most 7 partition pairs,
+        # so the stream pool never has to create streams while serving
+        b = adaptive32
+        modes.append(("nova_adaptive_g32", dict(mode="nova", decode_cus=(b["sm_op_v"], b["sm_op_p"]),
+                                                alpha=(b["alpha_v"], b["alpha_p"]), minimum=b["sm_min"], granule=32)))
+    return modes + [
+        ("time_sliced_decode_first", dict(mode="time_sliced", slice_order="decode_first")),
+        ("time_sliced_prefill_first", dict(mode="time_sliced", slice_order="prefill_first")),
+        ("pf_limit", dict(mode="time_sliced", slice_order="prefill_first", decode_limit=5)),
+        ("multi_stream", dict(mode="multi_stream"))]
 
 
 def run_serving(serve, sched, srv, curves, out_len, rates, seeds, window, modes=None, timeline_at=None):
@@ -277,12 +284,13 @@ def run_serving(serve, sched, srv, curves, out_len, rates, seeds, window, modes=
     over seeds, the better of the two time-sliced orders, and Eq. 6 beside the measured wait."""
     grid = sorted(set([0.25, 0.5, 1, 1.5, 2, 3, 4, 5, 6, 7, 8] + list(rates)))
     adaptive = sched.adaptive_params(curves, out_len, grid)
+    adaptive32 = sched.adaptive_params(curves, out_len, grid, granule=32) if modes and "nova_adaptive_g32" in modes else None
     log(f"adaptive Eq. 5 parameters: SM_op {adaptive['sm_op_v']}/{adaptive['sm_op_p']}, alpha "
         f"{adaptive['alpha_v']}/{adaptive['alpha_p']}, SM_min {adaptive['sm_min']}")
     runs = []
     for rate in rates:
         for seed in seeds:
-            for mode, kw in serving_modes(sched, curves, out_len, rate, adaptive):
+            for mode, kw in serving_modes(sched, curves, out_len, rate, adaptive, adaptive32):
                 if modes and mode not in modes:
                     continue
                 trace = serve.poisson_trace(rate, window, seed=seed)

@@ -96,16 +96,16 @@ class BlockPool:
 
 class Server:
     def __init__(self, vit, llm, kv, pixels, mode="nova", decode_cus=(96, 96), alpha=0, minimum=32, max_batch=32,
-                 max_blocks=256, device="cuda", slice_order="alternate", decode_limit=None):
+                 max_blocks=256, device="cuda", slice_order="alternate", decode_limit=None, granule=sched.GRANULE):
         """decode_cus = (P_v, P_p): decode's CUs while co-running with vision encode / prefill
         (Eq. 3's optimum); alpha > 0 (one value, or one per pair as (alpha_v, alpha_p)) turns on
-        the Eq. 5 adaptation with floor `minimum`.
+        the Eq. 5 adaptation with floor `minimum`, its shares rounded down to `granule` CUs.
         slice_order / decode_limit choose the time-sliced driver's pass order (see
         _slice_decode_next)."""
         if slice_order not in ("alternate", "decode_first", "prefill_first"):
             raise ValueError(f"unknown slice_order {slice_order!r}")
         self.vit, self.llm, self.kv, self.pixels, self.device = vit, llm, kv, pixels, device
-        self.mode, self.decode_cus, self.alpha, self.minimum = mode, decode_cus, alpha, minimum
+        self.mode, self.decode_cus, self.alpha, self.minimum, self.granule = mode, decode_cus, alpha, minimum, granule
         self.slice_order, self.decode_limit = slice_order, decode_limit
         self.other = None             # stage co-running with decode: STAGE_ENCODE, STAGE_PREFILL or None
         self.max_batch, self.max_blocks = max_batch, max_blocks
@@ -141,7 +141,7 @@ class Server:
         i = 0 if pair == nova.STAGE_ENCODE else 1
         op = self.decode_cus[i]
         alpha = self.alpha[i] if isinstance(self.alpha, (tuple, list)) else self.alpha
-        p = sched.decode_cus(pend, op, alpha, self.minimum) if alpha else op
+        p = sched.decode_cus(pend, op, alpha, self.minimum, self.granule) if alpha else op
         return nova.make_cu_mask(p, 0) if stage == nova.STAGE_DECODE else nova.make_cu_mask(256 - p, p // 8)
 
     def _stream(self, stage):
