@@ -705,6 +705,10 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         q.vt = nullptr;
         hipError_t e = launch_dma<float, EPI_STORE, 256, 256, 64, 128>(q, s, sl);
         if (e != hipSuccess) return e;
+        if (EPI == EPI_RESID && p.slices_out != nullptr && p.bias == nullptr) {   // the caller folds them
+          *p.slices_out = sl;
+          return hipSuccess;
+        }
         const long n4 = (long)p.M * (p.N / 4);
         hipLaunchKernelGGL((split_reduce_kernel<OT, EPI>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, p,
                            (const float*)p.split_ws, sl);
@@ -726,6 +730,10 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         q.vt = nullptr;
         hipError_t e = launch_dma<float, EPI_STORE, 128, 128, 64, 64>(q, s, sl);
         if (e != hipSuccess) return e;
+        if (EPI == EPI_RESID && p.slices_out != nullptr && p.bias == nullptr) {   // the caller folds them
+          *p.slices_out = sl;
+          return hipSuccess;
+        }
         const long n4 = (long)p.M * (p.N / 4);
         hipLaunchKernelGGL((split_reduce_kernel<OT, EPI>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, p,
                            (const float*)p.split_ws, sl);
@@ -764,6 +772,7 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
 
 template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s) {
+  if (p.slices_out != nullptr) *p.slices_out = 0;
   if (p.M <= 0) return hipSuccess;
   if (p.N % 128 || p.K % BK || p.lda % 8 || p.ldw % 8 || p.ldo % 4) return hipErrorInvalidValue;
   switch (epi) {

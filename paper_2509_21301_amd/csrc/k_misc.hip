@@ -18,14 +18,19 @@ namespace nova {
 constexpr int NORM_MAXV = 16;     // float4 per lane: H <= 64 * 4 * 16
 // NV: float4 per lane held in registers (the row width rounded up to 256 columns), as few as the
 // row needs so that more rows are in flight per CU
-template <typename T, int NV>
-__global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, int M, int H, const bf16_t* __restrict__ g,
+// RES: before the statistics, the row is updated in place with a residual branch that arrives as
+// `slices` fp32 K-slice partials (part + k * pstride, k = 0 .. slices-1, summed in slice order, as
+// split_reduce_kernel does): x += ((p_0 + p_1) + ...).  This folds the reduction pass of a K-split
+// residual projection into the norm that reads its output next.
+template <typename T, int NV, bool RES>
+__global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ x, int M, int H, const bf16_t* __restrict__ g,
                                                    const bf16_t* __restrict__ bb, float eps, int ln, T* __restrict__ out,
-                                                   int ldo, int merge, int gh, int gw) {
+                                                   int ldo, int merge, int gh, int gw, const float* __restrict__ part,
+                                                   int slices, size_t pstride) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
-  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)row * H);
+  float4* xr = reinterpret_cast<float4*>(x + (size_t)row * H);
   const int n4 = H / 4;
   float4 v[NV];
   float s = 0.f;
@@ -33,6 +38,18 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
   for (int j = 0; j < NV; ++j) {
     const int i = j * 64 + lane;
     v[j] = i < n4 ? xr[i] : float4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (RES) {
+      if (i < n4) {
+        const float4* pr = reinterpret_cast<const float4*>(part + (size_t)row * H) + i;
+        float4 d = pr[0];
+        for (int k = 1; k < slices; ++k) {
+          const float4 e = pr[k * (pstride / 4)];
+          d.x += e.x; d.y += e.y; d.z += e.z; d.w += e.w;
+        }
+        v[j] = float4{v[j].x + d.x, v[j].y + d.y, v[j].z + d.z, v[j].w + d.w};
+        xr[i] = v[j];
+      }
+    }
     s += v[j].x + v[j].y + v[j].z + v[j].w;
   }
   const float mean = ln ? wave_sum(s) / H : 0.f;
@@ -73,14 +90,16 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
   }
 }
 
-template <typename T>
-hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln, T* out,
-                     int ldo, int merge, int gh, int gw, hipStream_t s) {
+template <typename T, bool RES>
+static hipError_t norm_launch(float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln, T* out, int ldo,
+                              int merge, int gh, int gw, const float* part, int slices, size_t pstride, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (H % 4 || H > 4 * 64 * NORM_MAXV || ldo % 4) return hipErrorInvalidValue;
   const dim3 grid((M + 3) / 4);
   const int nv = (H + 255) / 256;
-#define NORM_LAUNCH(NVV) hipLaunchKernelGGL((norm_kernel<T, NVV>), grid, dim3(256), 0, s, x, M, H, g, b, eps, ln, out, ldo, merge, gh, gw)
+#define NORM_LAUNCH(NVV)                                                                                             \
+  hipLaunchKernelGGL((norm_kernel<T, NVV, RES>), grid, dim3(256), 0, s, x, M, H, g, b, eps, ln, out, ldo, merge, gh, gw, \
+                     part, slices, pstride)
   if (nv <= 1) NORM_LAUNCH(1);
   else if (nv <= 2) NORM_LAUNCH(2);
   else if (nv <= 4) NORM_LAUNCH(4);
@@ -90,6 +109,20 @@ hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t
   else NORM_LAUNCH(NORM_MAXV);
 #undef NORM_LAUNCH
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln, T* out,
+                     int ldo, int merge, int gh, int gw, hipStream_t s) {
+  // the plain norm never writes x
+  return norm_launch<T, false>(const_cast<float*>(x), M, H, g, b, eps, ln, out, ldo, merge, gh, gw, nullptr, 0, 0, s);
+}
+
+template <typename T>
+hipError_t split_norm_rows(const float* part, int slices, size_t pstride, float* x, int M, int H, const bf16_t* g,
+                           const bf16_t* b, float eps, int ln, T* out, int ldo, hipStream_t s) {
+  if (part == nullptr || slices < 1 || pstride < (size_t)M * H || pstride % 4) return hipErrorInvalidValue;
+  return norm_launch<T, true>(x, M, H, g, b, eps, ln, out, ldo, 1, 0, 0, part, slices, pstride, s);
 }
 
 // ------------------------------------------------------------------ patchify
@@ -466,6 +499,10 @@ hipError_t argmax_rows(const float* logits, int B, int V, int* out, hipStream_t 
 
 template hipError_t norm_rows<bf16_t>(const float*, int, int, const bf16_t*, const bf16_t*, float, int, bf16_t*, int, int, int, int, hipStream_t);
 template hipError_t norm_rows<float>(const float*, int, int, const bf16_t*, const bf16_t*, float, int, float*, int, int, int, int, hipStream_t);
+template hipError_t split_norm_rows<bf16_t>(const float*, int, size_t, float*, int, int, const bf16_t*, const bf16_t*, float, int,
+                                            bf16_t*, int, hipStream_t);
+template hipError_t split_norm_rows<float>(const float*, int, size_t, float*, int, int, const bf16_t*, const bf16_t*, float, int,
+                                           float*, int, hipStream_t);
 template hipError_t patchify<bf16_t>(const bf16_t*, int, int, int, int, int, bf16_t*, hipStream_t);
 template hipError_t patchify<float>(const bf16_t*, int, int, int, int, int, float*, hipStream_t);
 template <typename T>

@@ -38,6 +38,10 @@ struct GemmArgs {
   // bf16 only: always 128x128 tiles of 4 waves, unsplit (a kernel that leaves room on every CU for
   // another kernel's workgroups: the intra-CU co-residency variant)
   bool small_tiles = false;
+  // RESID without bias only: when set and K is split, the K-slice partials are left in split_ws
+  // ([slices][M][N]) for the caller to fold into out (split_norm_rows), and *slices_out gets the
+  // slice count; otherwise *slices_out = 0 and out is complete
+  int* slices_out = nullptr;
 };
 template <typename TA, typename OT>
 hipError_t gemm(const GemmArgs& p, int epi, hipStream_t s);
@@ -132,6 +136,12 @@ hipError_t gemv_valu(const bf16_t* X, int ldx, const bf16_t* W, int ldw, int B, 
 template <typename T>
 hipError_t norm_rows(const float* x, int M, int H, const bf16_t* g, const bf16_t* b, float eps, int ln,
                      T* out, int ldo, int merge, int gh, int gw, hipStream_t s);
+// The same norm after folding a K-split residual projection into x: x[m] += the sum of the
+// `slices` fp32 partials part[k * pstride + m * H + n] in slice order (pstride >= M * H), written
+// back, then the norm of the updated rows into out (merge 1).  The partials carry no bias.
+template <typename T>
+hipError_t split_norm_rows(const float* part, int slices, size_t pstride, float* x, int M, int H, const bf16_t* g,
+                           const bf16_t* b, float eps, int ln, T* out, int ldo, hipStream_t s);
 // Image [B, H, W, 3] bf16 -> patch rows [B*gh*gw, kpad] (zero padded), order (py, px, c).
 template <typename T>
 hipError_t patchify(const bf16_t* img, int B, int H, int W, int p, int kpad, T* out, hipStream_t s);

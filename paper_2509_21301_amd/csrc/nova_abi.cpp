@@ -679,12 +679,26 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
   };
 
   CALL(NOVA_KIND_MISC, s, nova::embed_rows<T>(vis, n_vis, ids, n_text, (const bf16_t*)m->d.embed, H, x, s));
+  // a residual projection (O, down) whose K is split leaves its slices for the RMSNorm that reads
+  // x next to fold in (one pass over x instead of a reduction pass and a norm pass)
+  auto resid_then_norm = [&](const GemmArgs& g, const bf16_t* gain) -> int {
+    GemmArgs p = g;
+    int slices = 0;
+    p.slices_out = &slices;
+    CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
+    if (slices > 0)
+      CALL(NOVA_KIND_MISC, s, nova::split_norm_rows<T>(split_ws, slices, (size_t)S * H, x, S, H, gain, nullptr, c.eps, 0, a, H, s));
+    else
+      CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, S, H, gain, nullptr, c.eps, 0, a, H, 1, 0, 0, s));
+    return (int)NOVA_OK;
+  };
   for (int l = 0; l < c.layers; ++l) {
     const char* lw = (const char*)m->d.layers + (size_t)l * m->lay.bytes;
     auto W = [&](int i) { return (const bf16_t*)(lw + m->lay.off[i]); };
     T* kp = (T*)kv->k + l * kv_layer;
     T* vp = (T*)kv->v + l * kv_layer;
-    CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, S, H, W(0), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
+    if (l == 0)      // later layers: the previous layer's down projection normalised x already
+      CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, S, H, W(0), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
     {
       const GemmArgs p = with_split(GemmArgs{a, H, W(1), H, S, m->qkvw, H, nullptr, qkv, m->qkvw, nullptr, 0});
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_STORE, s)));
@@ -694,18 +708,20 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
       nova::AttnArgs p{qkv, m->qkvw, 0, qkv + qd, m->qkvw, 0, vt, skp, att, qd, 0, S, S, c.n_q, c.n_kv, 1, 1};
       CALL(NOVA_KIND_ATTN, s, nova::attention<T>(p, D, s));
     }
-    {
-      const GemmArgs p = with_split(GemmArgs{att, qd, W(2), qd, S, H, qd, nullptr, x, H, nullptr, 0});
-      CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
-    }
-    CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, S, H, W(3), nullptr, c.eps, 0, a, H, 1, 0, 0, s));
+    if (int rc = resid_then_norm(with_split(GemmArgs{att, qd, W(2), qd, S, H, qd, nullptr, x, H, nullptr, 0}), W(3)))
+      return rc;
     {
       GemmArgs p{a, H, W(4), H, S, 2 * m->ip, H, nullptr, hm, m->ip, nullptr, 0};
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_SWIGLU, s)));
     }
     {
       const GemmArgs p = with_split(GemmArgs{hm, m->ip, W(5), m->ip, S, H, m->ip, nullptr, x, H, nullptr, 0});
-      CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
+      if (l + 1 < c.layers) {   // with the next layer's input norm
+        const bf16_t* next_gain = (const bf16_t*)((const char*)m->d.layers + (size_t)(l + 1) * m->lay.bytes + m->lay.off[0]);
+        if (int rc = resid_then_norm(p, next_gain)) return rc;
+      } else {                  // the last layer: the final norm reads the last row only
+        CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
+      }
     }
   }
   const char* hw = (const char*)m->d.head;
