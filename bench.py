@@ -544,8 +544,8 @@ def cpu_baseline(synth):
       extrapolated to a full pass (the headline unit, patches/s);
     * prefill: one of the 28 decoder layers over the 1500-token prompt plus the LM head on a
       1/16 slice of the vocabulary, extrapolated to 28 layers and the full head (tok/s);
-    * decode: one batch-1 step through one layer at a 1500-token context, and the head slice,
-      extrapolated the same way (tok/s);
+    * decode: one step of batch 1, 8 and 32 through one layer at a 1500-token context, and the
+      head slice, extrapolated the same way (tok/s);
     * the tiny stack end to end (encode, 96-token prefill, 16 greedy decode steps)."""
     import dataclasses
     from oracle import vlm
@@ -593,7 +593,22 @@ def cpu_baseline(synth):
     vlm.llm_decode_step(np.array([5]), np.array([s]), tables, kv, wl, l1)
     t_dec1 = time.perf_counter() - t0
     t_decode = lc.layers * t_dec1 + t_head          # the slice's head time is inside t_dec1; upper bound
-    del wl, kv
+    del kv
+    # batches of 8 and 32 sequences at the same context, the same way (head on B rows, scaled up)
+    t_dec_b = {}
+    for bsz in (8, 32):
+        tb, pb = synth.block_tables([s + 1] * bsz, lc.block, seed=5)
+        kvb = vlm.PagedKV(1, pb, lc.n_kv, lc.block, lc.head_dim)
+        kvb.k[:] = rng.standard_normal(kvb.k.shape)
+        kvb.v[:] = rng.standard_normal(kvb.v.shape)
+        t0 = time.perf_counter()
+        vlm.llm_decode_step(np.full(bsz, 5), np.full(bsz, s), tb, kvb, wl, l1)
+        t_step = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        vlm.lm_head(np.repeat(h[-1:], bsz, 0), wl, l1)
+        t_dec_b[bsz] = lc.layers * t_step + (time.perf_counter() - t0) * (lc.vocab / vs)
+        del kvb
+    del wl
     # tiny stack end to end
     tv, tl = synth.TINY_VIT, synth.TINY_LLM
     wv, wt = synth.vit_weights(tv, 0), synth.llm_weights(tl, 0)
@@ -616,6 +631,8 @@ def cpu_baseline(synth):
             "stages": {"encode_image_s": round(t_img, 2),
                        "prefill_s1500_s": round(t_prefill, 2), "prefill_tok_per_s": round(s / t_prefill, 2),
                        "decode_b1_step_s": round(t_decode, 3), "decode_b1_tok_per_s": round(1 / t_decode, 3),
+                       "decode_b8_step_s": round(t_dec_b[8], 3), "decode_b8_tok_per_s": round(8 / t_dec_b[8], 3),
+                       "decode_b32_step_s": round(t_dec_b[32], 3), "decode_b32_tok_per_s": round(32 / t_dec_b[32], 3),
                        "tiny_stack_end_to_end_s": round(t_tiny, 3),
                        "note": "prefill and decode: 1 of 28 layers timed and the LM head on 1/16 of the "
                                "vocabulary, extrapolated to 28 layers and the full head"}}
