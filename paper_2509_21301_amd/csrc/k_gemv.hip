@@ -74,6 +74,7 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
   __shared__ __align__(16) bf16_t xs[XR * XSLOT];
   __shared__ float red[EPI == EPI_RESID ? 4 : 1][32];     // per-wave row statistics (residual producers)
   __shared__ float rstd_s[NSCALE ? 32 : 1];                // per-row RMSNorm scale (normalising consumers)
+  __shared__ unsigned long long am_s[EPI == EPI_ARGMAX ? 4 : 1][16];   // per-wave argmax keys
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_base = blockIdx.x * GV_ROWS + wave * GV_RW;
@@ -239,7 +240,20 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p, int kc) {
         const unsigned long long other = __shfl_xor(key, o, 64);
         key = other > key ? other : key;
       }
-      if (lane < 16 && b < p.B) atomicMax(p.argmax_keys + b, key);
+      // the workgroup's 4 waves combine through LDS, and one lane per row merges the result only
+      // if it beats the row's best so far (which only grows, so a stale read merely costs an
+      // extra atomic): some 2400 workgroups of the LM head would otherwise queue 4 atomics each
+      // on the same address (a fifth of the head's time)
+      if (lane < 16) am_s[wave][lane] = key;
+      __syncthreads();
+      if (wave == 0 && lane < 16 && b < p.B) {
+        unsigned long long k = am_s[0][lane];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) k = am_s[w][lane] > k ? am_s[w][lane] : k;
+        if (k > __hip_atomic_load(p.argmax_keys + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+          atomicMax(p.argmax_keys + b, k);
+      }
+      __syncthreads();          // am_s is reused by the next column group
       continue;
     }
 #pragma unroll
