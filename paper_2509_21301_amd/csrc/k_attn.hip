@@ -17,6 +17,8 @@
 //    three significant cross products are accumulated;
 //  * bidirectional bf16 with head_dim <= 80 (the vision encoder) runs a wider variant: two query
 //    groups per wave share every fragment read, and the row sums come out of the P V^T MFMAs.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -59,10 +61,29 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_kernel(AttnArgs p) {
   // head) pairs split evenly over the XCDs each XCD takes whole pairs, one after another, and the
   // pair's K and V stay in its L2 while all of the pair's query blocks read them
   int qbi, h, b;
+  int pair, part = 0, nparts = 1, slot = 0;
   {
-    const int pairs = p.batch * p.n_q, lin = blockIdx.x;
-    int pair;
-    if (CAUSAL) {
+    const int pairs = p.batch * p.n_q;
+    int lin = blockIdx.x;
+    if (CAUSAL && p.kv_tmax > 0) {
+      // key ranges: query block q is cut into P(q) = ceil(tiles(q) / kv_tmax) ranges of whole
+      // tiles.  The grid runs level by level from the heaviest block down, each level holding
+      // every pair's ranges of that block (range-major); a multi-range block's partials take
+      // P(q) consecutive slots of its pair's kv_slots
+      int units = 0, slots = 0, q = nqb - 1, P = 1;
+      for (;; --q) {
+        P = ((min(p.sk, (q + 1) * AQB) + AK - 1) / AK + p.kv_tmax - 1) / p.kv_tmax;
+        if (lin < (units + P) * pairs || q == 0) break;
+        units += P;
+        if (P > 1) slots += P;
+      }
+      lin -= units * pairs;
+      qbi = nqb - 1 - q;
+      nparts = P;
+      part = lin / pairs;
+      pair = lin - part * pairs;
+      slot = pair * p.kv_slots + p.kv_slots - slots - (P > 1 ? P : 0) + part;
+    } else if (CAUSAL) {
       // heaviest blocks of every head first: the workgroups dispatched last, which share a CU
       // with an earlier one, are the lightest; head h's blocks fall on XCDs (h + pairs k) % 8
       qbi = lin / pairs;
@@ -182,13 +203,19 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_kernel(AttnArgs p) {
   const float scale = 1.4426950408889634f / sqrtf((float)D);
 
   const int kv_end = CAUSAL ? min(p.sk, q0 + AQB) : p.sk;
+  int kv_lo = 0, kv_hi = kv_end;
+  if (CAUSAL && nparts > 1) {     // this workgroup's range: whole tiles, as even as they split
+    const int per = ((kv_end + AK - 1) / AK + nparts - 1) / nparts;
+    kv_lo = part * per * AK;
+    kv_hi = min(kv_end, kv_lo + per * AK);
+  }
   const int wave_qmax = q0 + wave * 32 + 31;
-  load_tile(0);
-  for (int kv0 = 0; kv0 < kv_end; kv0 += AK) {
+  load_tile(kv_lo);
+  for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += AK) {
     __syncthreads();          // previous tile fully consumed
     store_tile();
     __syncthreads();
-    if (kv0 + AK < kv_end) load_tile(kv0 + AK);
+    if (kv0 + AK < kv_hi) load_tile(kv0 + AK);
     if (CAUSAL && kv0 > wave_qmax) continue;   // every key of this tile is in this wave's future
 
     // S^T = K Q^T for two 32-key blocks
@@ -278,6 +305,70 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_kernel(AttnArgs p) {
           }
         }
       }
+  }
+
+  if (CAUSAL && nparts > 1) {
+    // Every range stores its unnormalised output, running max and sum (fp32, [value][thread] per
+    // slot) with device-scope atomic stores, written through to the coherent level; every thread
+    // waits until its stores are acknowledged there before the workgroup barrier, and only then
+    // does thread 0 count the range in.  The last range of the block to arrive reads the others
+    // back with device-scope atomic loads and merges all of them in range order, so the result
+    // does not depend on which range finished last.
+    constexpr int PV = NC * 16 + 2;
+    float* po = reinterpret_cast<float*>(p.part);
+    auto at = [&](int sl, int v) { return po + ((size_t)sl * PV + v) * NT + tid; };
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) __hip_atomic_store(at(slot, c * 16 + r), o[c][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(at(slot, NC * 16), m_run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(at(slot, NC * 16 + 1), l_run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __shared__ int last;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    unsigned* cnt = p.counters + (size_t)pair * nqb + qb;
+    if (tid == 0) last = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(nparts - 1);
+    __syncthreads();
+    if (!last) return;
+    if (tid == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int s0 = slot - part;
+    float mk[8], mmax = -1e30f;       // at most 8 ranges (the launcher's bound)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      mk[k] = k >= nparts ? -1e30f : k == part ? m_run : __hip_atomic_load(at(s0 + k, NC * 16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      mmax = fmaxf(mmax, mk[k]);
+    }
+    f32x16 acc[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c] = f32x16{};
+    float lsum = 0.f;
+    for (int k = 0; k < nparts; ++k) {
+      float w = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) w = j == k ? mk[j] : w;
+      w = __builtin_amdgcn_exp2f((w - mmax) * scale);
+      if (k == part) {
+        lsum += w * l_run;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[c][r] += w * o[c][r];
+      } else {
+        lsum += w * __hip_atomic_load(at(s0 + k, NC * 16 + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        float t[NC][16];
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) t[c][r] = __hip_atomic_load(at(s0 + k, c * 16 + r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[c][r] += w * t[c][r];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) o[c] = acc[c];
+    l_run = lsum;
   }
 
   if (qrow >= p.sq) return;
@@ -731,6 +822,42 @@ static int wide_kv_parts(const AttnArgs& p, int D) {
   return best;
 }
 
+// Key ranges of the causal kernel.  A causal query block of 128 reads every key up to its own
+// last query, so the heaviest blocks take as many tiles as the sequence has, and on their own set
+// the launch's length when all blocks run at once.  When the (pair, block) workgroups fit in one
+// round of the GPU's workgroup slots (two per CU), the blocks are cut into ranges of at most tmax
+// tiles, tmax the smallest (at least 4) that keeps the ranges within that one round, with at most
+// 8 ranges per block and the fp32 partials within p.part.  A second round, or more partials,
+// cost more than the shorter ranges save (the 1500-token prefill: attention 1.44 ms per pass
+// unsplit, 1.13 ms in one round of ranges of 12 tiles, 1.38-1.45 ms with ranges of 4-8 tiles
+// over two rounds; the 3579-token one, already past one round unsplit: 3.55 ms, 4.3-5.2 ms cut).
+// Returns the ranges per pair (the grid is that times the pairs), or 0 when no block is cut
+// (q.kv_tmax = 0).
+template <int D>
+static int causal_key_ranges(AttnArgs& q, int qblock, int threads) {
+  q.kv_tmax = 0;
+  if (q.part == nullptr || q.counters == nullptr || q.batch <= 0 || q.n_q <= 0) return 0;
+  const int nqb = (q.sq + qblock - 1) / qblock, pairs = q.batch * q.n_q;
+  const long slots_gpu = 2L * (q.cus > 0 ? q.cus : 256);
+  if ((long)nqb * pairs > slots_gpu) return 0;
+  auto tiles = [&](int qb) { return (std::min(q.sk, (qb + 1) * qblock) + AK - 1) / AK; };
+  const int most = tiles(nqb - 1);
+  constexpr size_t PV = (D + 31) / 32 * 16 + 2;        // fp32 values per thread and range
+  for (int tmax = 4; tmax < most; ++tmax) {
+    if ((most + tmax - 1) / tmax > 8) continue;
+    int units = 0, slots = 0;
+    for (int qb = 0; qb < nqb; ++qb) {
+      const int P = (tiles(qb) + tmax - 1) / tmax;
+      units += P;
+      if (P > 1) slots += P;
+    }
+    if ((long)units * pairs > slots_gpu || (size_t)pairs * slots * PV * threads * sizeof(float) > q.part_bytes) continue;
+    q.kv_tmax = tmax, q.kv_units = units, q.kv_slots = slots;
+    return units;
+  }
+  return 0;
+}
+
 template <typename T, int D>
 static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
   if constexpr (sizeof(T) == 2 && D <= 80) {
@@ -751,8 +878,10 @@ static hipError_t attn_launch(const AttnArgs& p, hipStream_t s) {
     // against 51 us per layer on the 1500-token prefill (twice the K/V staging per query, and the
     // staging registers spill)
     constexpr int NW = 4;
-    hipLaunchKernelGGL((attn_kernel<T, D, true, NW>), dim3((p.sq + NW * 32 - 1) / (NW * 32) * p.n_q * p.batch),
-                       dim3(NW * 64), 0, s, p);
+    AttnArgs q = p;
+    int units = causal_key_ranges<D>(q, NW * 32, NW * 64);
+    if (units == 0) units = (p.sq + NW * 32 - 1) / (NW * 32);
+    hipLaunchKernelGGL((attn_kernel<T, D, true, NW>), dim3(units * p.n_q * p.batch), dim3(NW * 64), 0, s, q);
   } else {
     hipLaunchKernelGGL((attn_kernel<T, D, false, 4>), dim3((p.sq + AQ - 1) / AQ * p.n_q * p.batch), dim3(256), 0, s, p);
   }

@@ -168,8 +168,10 @@ template <typename T>
 __global__ void __launch_bounds__(256) qkv_prefill_kernel(T* __restrict__ qkv, int S, int n_q, int n_kv, int D, float theta,
                                                           int pos0, T* __restrict__ vt, int sk_pad, T* __restrict__ kpool,
                                                           T* __restrict__ vpool, const int* __restrict__ table, int block,
-                                                          int h0) {
+                                                          int h0, unsigned* __restrict__ zero, int nzero) {
   constexpr int EPC = 16 / sizeof(T);      // elements per 16-byte piece
+  if (zero != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0)
+    for (int i = threadIdx.x; i < nzero; i += 256) zero[i] = 0u;
   constexpr int TP = 128 + EPC;            // tile pitch (elements), D <= 128
   __shared__ __align__(16) T tile[64 * TP];
   __shared__ double inv_s[64];             // D / 2 <= 64
@@ -255,7 +257,8 @@ __global__ void __launch_bounds__(256) qkv_prefill_kernel(T* __restrict__ qkv, i
 
 template <typename T>
 hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0, T* vt,
-                       int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s) {
+                       int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s, unsigned* zero,
+                       int nzero) {
   if (S <= 0) return hipSuccess;
   if (D > 128 || D % 16 || sk_pad < S || sk_pad % 64) return hipErrorInvalidValue;
   if (table != nullptr && block % (16 / (int)sizeof(T))) return hipErrorInvalidValue;
@@ -263,7 +266,7 @@ hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float
   const int h0 = rope_theta > 0.f || table != nullptr ? 0 : n_q + n_kv;
   dim3 grid(sk_pad / 64, n_q + 2 * n_kv - h0, batch);
   hipLaunchKernelGGL((qkv_prefill_kernel<T>), grid, dim3(256), 0, s, qkv, S, n_q, n_kv, D, rope_theta, pos0, vt, sk_pad,
-                     kpool, vpool, table, block, h0);
+                     kpool, vpool, table, block, h0, zero, nzero);
   return hipGetLastError();
 }
 
@@ -523,8 +526,8 @@ hipError_t zero_tail_cols(T* buf, long rows, int ld, int c0, hipStream_t s) {
 template hipError_t zero_tail_cols<bf16_t>(bf16_t*, long, int, int, hipStream_t);
 template hipError_t zero_tail_cols<float>(float*, long, int, int, hipStream_t);
 
-template hipError_t qkv_prefill<bf16_t>(bf16_t*, int, int, int, int, int, float, int, bf16_t*, int, bf16_t*, bf16_t*, const int*, int, hipStream_t);
-template hipError_t qkv_prefill<float>(float*, int, int, int, int, int, float, int, float*, int, float*, float*, const int*, int, hipStream_t);
+template hipError_t qkv_prefill<bf16_t>(bf16_t*, int, int, int, int, int, float, int, bf16_t*, int, bf16_t*, bf16_t*, const int*, int, hipStream_t, unsigned*, int);
+template hipError_t qkv_prefill<float>(float*, int, int, int, int, int, float, int, float*, int, float*, float*, const int*, int, hipStream_t, unsigned*, int);
 template hipError_t resid_rmsnorm<bf16_t>(const float*, int, float*, int, int, const bf16_t*, float, bf16_t*, int, unsigned long long*, hipStream_t);
 template hipError_t resid_rmsnorm<float>(const float*, int, float*, int, int, const bf16_t*, float, float*, int, unsigned long long*, hipStream_t);
 template hipError_t resid_fold<bf16_t>(const float*, int, float*, int, int, const bf16_t*, bf16_t*, int, float*,

@@ -103,6 +103,11 @@ struct AttnArgs {
   void* part = nullptr; size_t part_bytes = 0;
   int cus = 0;                // compute units of the stream (0: all 256)
   int kv_parts = 1;           // set by the launcher
+  // optional (causal bf16): with part and counters ([batch * n_q][query blocks of 128], zero on
+  // entry, zero again on return), the heaviest query blocks are cut into key ranges whose fp32
+  // partials land in part; the last range of a block to finish merges them
+  unsigned* counters = nullptr;
+  int kv_tmax = 0, kv_units = 0, kv_slots = 0;   // set by the launcher
 };
 template <typename T>
 hipError_t attention(const AttnArgs& p, int head_dim, hipStream_t s);
@@ -151,9 +156,11 @@ hipError_t zero_tail_cols(T* buf, long rows, int ld, int c0, hipStream_t s);
 // Split a packed QKV projection.  Rotates q and k in place when rope_theta > 0 (positions
 // pos0 + t), writes V transposed for attention (vt), and when tables != null writes the
 // rotated K and V of every token into the paged cache.
+// zero != null: also sets zero[0 .. nzero) to 0 (the attention's arrival counters).
 template <typename T>
 hipError_t qkv_prefill(T* qkv, int S, int batch, int n_q, int n_kv, int D, float rope_theta, int pos0,
-                       T* vt, int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s);
+                       T* vt, int sk_pad, T* kpool, T* vpool, const int* table, int block, hipStream_t s,
+                       unsigned* zero = nullptr, int nzero = 0);
 // Decode residual + RMSNorm, one workgroup per row: x[b] += sum_s partial[s][b] (if splits > 0),
 // then a[b] = x[b] / sqrt(mean(x[b]^2) + eps) * g.
 // keys != null: also zero keys[b] for the fused argmax of the projection that follows.

@@ -593,6 +593,7 @@ size_t prefill_ws(const nova_llm* m, int S, Carve* cv) {
   w.take<T>((size_t)S * m->ip);                                  // MLP hidden
   w.take<unsigned long long>(1);                                 // argmax key
   w.take<float>(prefill_split_floats(m, S));                     // split-K partials
+  w.take<unsigned>((size_t)c.n_q * ((S + 127) / 128));           // attention arrival counters
   return w.used;
 }
 template <typename T>
@@ -669,6 +670,8 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
   unsigned long long* keys = w.take<unsigned long long>(1);
   const size_t split_floats = prefill_split_floats(m, S);
   float* split_ws = w.take<float>(split_floats);
+  const int n_cnt = c.n_q * ((S + 127) / 128);
+  unsigned* att_cnt = w.take<unsigned>((size_t)n_cnt);
   const size_t kv_layer = (size_t)kv->num_blocks * c.n_kv * c.block * D;
   const int cus = stream_cus(s);
   // the QKV, O and down projections may split K when their tiles cannot fill the GPU
@@ -703,9 +706,13 @@ int llm_prefill_t(const nova_llm* m, const T* vis, int n_vis, const int* ids, in
       const GemmArgs p = with_split(GemmArgs{a, H, W(1), H, S, m->qkvw, H, nullptr, qkv, m->qkvw, nullptr, 0});
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_STORE, s)));
     }
-    CALL(NOVA_KIND_MISC, s, nova::qkv_prefill<T>(qkv, S, 1, c.n_q, c.n_kv, D, c.rope_theta, 0, vt, skp, kp, vp, table, c.block, s));
+    CALL(NOVA_KIND_MISC, s, nova::qkv_prefill<T>(qkv, S, 1, c.n_q, c.n_kv, D, c.rope_theta, 0, vt, skp, kp, vp, table,
+                                                  c.block, s, att_cnt, n_cnt));
     {
       nova::AttnArgs p{qkv, m->qkvw, 0, qkv + qd, m->qkvw, 0, vt, skp, att, qd, 0, S, S, c.n_q, c.n_kv, 1, 1};
+      // the split-K partials are free between the QKV and O projections: the attention's key
+      // ranges keep theirs there
+      p.part = split_ws, p.part_bytes = split_floats * sizeof(float), p.counters = att_cnt, p.cus = cus;
       CALL(NOVA_KIND_ATTN, s, nova::attention<T>(p, D, s));
     }
     if (int rc = resid_then_norm(with_split(GemmArgs{att, qd, W(2), qd, S, H, qd, nullptr, x, H, nullptr, 0}), W(3)))
