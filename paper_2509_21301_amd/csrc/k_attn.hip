@@ -829,8 +829,10 @@ static int wide_kv_parts(const AttnArgs& p, int D) {
 // tiles, tmax the smallest (at least 4) that keeps the ranges within that one round, with at most
 // 8 ranges per block and the fp32 partials within p.part.  A second round, or more partials,
 // cost more than the shorter ranges save (the 1500-token prefill: attention 1.44 ms per pass
-// unsplit, 1.13 ms in one round of ranges of 12 tiles, 1.38-1.45 ms with ranges of 4-8 tiles
-// over two rounds; the 3579-token one, already past one round unsplit: 3.55 ms, 4.3-5.2 ms cut).
+// unsplit, 1.09-1.13 ms in one round of ranges of 12 tiles, 1.16-1.21 ms with 10, 14 or 16 tiles,
+// 1.38-1.45 ms with 4-8 tiles over two rounds; the 3579-token one, already past one round
+// unsplit: 3.36-3.55 ms, 3.79 ms with only its 6 heaviest blocks per head cut in two, up to
+// 5.2 ms cut finer: a cut block's merge lands on the end of the longest chain).
 // Returns the ranges per pair (the grid is that times the pairs), or 0 when no block is cut
 // (q.kv_tmax = 0).
 template <int D>
