@@ -16,7 +16,10 @@
 //  * fp32 mode (tiny-stack exact mode): q, k, v, p are split into bf16 hi + lo parts and the
 //    three significant cross products are accumulated;
 //  * bidirectional bf16 with head_dim <= 80 (the vision encoder) runs a wider variant: two query
-//    groups per wave share every fragment read, and the row sums come out of the P V^T MFMAs.
+//    groups per wave share every fragment read, and the row sums come out of the P V^T MFMAs;
+//  * causal: when all (head, query block) workgroups fit in one round of workgroup slots, the
+//    heaviest blocks are cut into key ranges whose fp32 partials the last range to finish merges,
+//    so the longest chain of key tiles is not the whole sequence.
 #include <algorithm>
 
 #include "common.hpp"
