@@ -390,27 +390,39 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) d
   }
 }
 
-// Log-sum-exp combine of the context splits: one workgroup of D threads per (sequence, head);
-// split statistics are read in parallel, then every thread sums its dimension over the splits.
+// Log-sum-exp combine of the context splits: one workgroup of D threads per (sequence, head).
+// Every load is issued before any is used (the first 16 splits' outputs of the thread's dimension,
+// and in wave 0 each split's max and sum), so the kernel waits for one round trip to memory
+// rather than three; every thread then sums its dimension over the splits in split order.
 template <typename T, int D>
 __global__ void __launch_bounds__(D) dec_attn_combine(DecAttnArgs p, int nsplit) {
+  constexpr int PF = 16;
   __shared__ float wts[64];
   __shared__ float norm;
   const int bh = blockIdx.x;                 // b * n_q + head
   const float* part = p.partial + (size_t)bh * nsplit * (D + 2);
   const int t = threadIdx.x;
-  float m = -1e30f;
-  if (t < nsplit) m = part[t * (D + 2)];
+  float ov[PF];
+#pragma unroll
+  for (int sp = 0; sp < PF; ++sp) ov[sp] = sp < nsplit ? part[sp * (D + 2) + 2 + t] : 0.f;
+  float m = -1e30f, l = 0.f;
+  if (t < nsplit) {
+    m = part[t * (D + 2)];
+    l = part[t * (D + 2) + 1];
+  }
   float M = wave_max(t < 64 ? m : -1e30f);
   if (t < 64) {
     const float w = t < nsplit ? exp2f(m - M) : 0.f;
-    const float lw = wave_sum(t < nsplit ? w * part[t * (D + 2) + 1] : 0.f);
+    const float lw = wave_sum(t < nsplit ? w * l : 0.f);
     wts[t] = w;
     if (t == 0) norm = 1.0f / lw;
   }
   __syncthreads();
   float O = 0.f;
-  for (int sp = 0; sp < nsplit; ++sp) O += wts[sp] * part[sp * (D + 2) + 2 + t];
+#pragma unroll
+  for (int sp = 0; sp < PF; ++sp)
+    if (sp < nsplit) O += wts[sp] * ov[sp];
+  for (int sp = PF; sp < nsplit; ++sp) O += wts[sp] * part[sp * (D + 2) + 2 + t];
   reinterpret_cast<T*>(p.out)[(size_t)bh * D + t] = from_f<T>(O * norm);
 }
 
