@@ -32,26 +32,51 @@ __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ x, int M,
   if (row >= M) return;
   float4* xr = reinterpret_cast<float4*>(x + (size_t)row * H);
   const int n4 = H / 4;
+  // every load of a phase is issued before any of its values is used: the gain (and, without a
+  // residual branch, the shift), x and the first partial slice together, then each further
+  // slice; a load issued after a store of x would wait for the stores before it (one round trip
+  // to memory per chunk)
+  uint2 gg[NV], bs[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = j * 64 + lane;
+    gg[j] = i < n4 ? *reinterpret_cast<const uint2*>(g + 4 * i) : make_uint2(0u, 0u);
+    if constexpr (!RES) bs[j] = ln && i < n4 ? *reinterpret_cast<const uint2*>(bb + 4 * i) : make_uint2(0u, 0u);
+  }
   float4 v[NV];
-  float s = 0.f;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int i = j * 64 + lane;
     v[j] = i < n4 ? xr[i] : float4{0.f, 0.f, 0.f, 0.f};
-    if constexpr (RES) {
-      if (i < n4) {
-        const float4* pr = reinterpret_cast<const float4*>(part + (size_t)row * H) + i;
-        float4 d = pr[0];
-        for (int k = 1; k < slices; ++k) {
-          const float4 e = pr[k * (pstride / 4)];
-          d.x += e.x; d.y += e.y; d.z += e.z; d.w += e.w;
-        }
-        v[j] = float4{v[j].x + d.x, v[j].y + d.y, v[j].z + d.z, v[j].w + d.w};
-        xr[i] = v[j];
-      }
-    }
-    s += v[j].x + v[j].y + v[j].z + v[j].w;
   }
+  if constexpr (RES) {
+    const float4* pr = reinterpret_cast<const float4*>(part + (size_t)row * H);
+    float4 d[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int i = j * 64 + lane;
+      d[j] = i < n4 ? pr[i] : float4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int k = 1; k < slices; ++k) {
+      float4 e[NV];
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        const int i = j * 64 + lane;
+        e[j] = i < n4 ? pr[k * (pstride / 4) + i] : float4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int j = 0; j < NV; ++j) d[j] = float4{d[j].x + e[j].x, d[j].y + e[j].y, d[j].z + e[j].z, d[j].w + e[j].w};
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int i = j * 64 + lane;
+      v[j] = float4{v[j].x + d[j].x, v[j].y + d[j].y, v[j].z + d[j].z, v[j].w + d[j].w};
+      if (i < n4) xr[i] = v[j];
+    }
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) s += v[j].x + v[j].y + v[j].z + v[j].w;
   const float mean = ln ? wave_sum(s) / H : 0.f;
   float ss = 0.f;
 #pragma unroll
@@ -74,11 +99,10 @@ __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ x, int M,
   for (int j = 0; j < NV; ++j) {
     const int i = j * 64 + lane;
     if (i >= n4) continue;
-    const uint2 gg = *reinterpret_cast<const uint2*>(g + 4 * i);
-    float y[4] = {(v[j].x - mean) * rstd * bf2f((bf16_t)(gg.x & 0xffff)), (v[j].y - mean) * rstd * bf2f((bf16_t)(gg.x >> 16)),
-                  (v[j].z - mean) * rstd * bf2f((bf16_t)(gg.y & 0xffff)), (v[j].w - mean) * rstd * bf2f((bf16_t)(gg.y >> 16))};
+    float y[4] = {(v[j].x - mean) * rstd * bf2f((bf16_t)(gg[j].x & 0xffff)), (v[j].y - mean) * rstd * bf2f((bf16_t)(gg[j].x >> 16)),
+                  (v[j].z - mean) * rstd * bf2f((bf16_t)(gg[j].y & 0xffff)), (v[j].w - mean) * rstd * bf2f((bf16_t)(gg[j].y >> 16))};
     if (ln) {
-      const uint2 b2 = *reinterpret_cast<const uint2*>(bb + 4 * i);
+      const uint2 b2 = RES ? *reinterpret_cast<const uint2*>(bb + 4 * i) : bs[j];
       y[0] += bf2f((bf16_t)(b2.x & 0xffff)); y[1] += bf2f((bf16_t)(b2.x >> 16));
       y[2] += bf2f((bf16_t)(b2.y & 0xffff)); y[3] += bf2f((bf16_t)(b2.y >> 16));
     }
@@ -325,6 +349,9 @@ __global__ void __launch_bounds__(256) resid_fold_kernel(const float* __restrict
   const int c = blockIdx.x * 64 + (t & 31) * 2;
   float sq = 0.f;
   if (b < B) {
+    // the gain pair is loaded with x and the partials (the compiler would otherwise issue it
+    // after the store of x, a second round trip to memory)
+    const uint32_t gp = *reinterpret_cast<const uint32_t*>(g + c);
     float* xp = x + (size_t)b * H + c;
     float2 v = *reinterpret_cast<const float2*>(xp);
     if (splits > 0) {
@@ -341,8 +368,8 @@ __global__ void __launch_bounds__(256) resid_fold_kernel(const float* __restrict
     }
     sq = v.x * v.x + v.y * v.y;
     T* ap = a + (size_t)b * lda + c;
-    ap[0] = from_f<T>(v.x * bf2f(g[c]));
-    ap[1] = from_f<T>(v.y * bf2f(g[c + 1]));
+    ap[0] = from_f<T>(v.x * __uint_as_float(gp << 16));
+    ap[1] = from_f<T>(v.y * __uint_as_float(gp & 0xffff0000u));
   }
 #pragma unroll
   for (int o = 16; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
