@@ -659,14 +659,16 @@ def main():
     ap.add_argument("--linear-corun", action="store_true",
                     help="only the two-linear co-run study (inter-CU partitions vs intra-CU sharing; prints its JSON)")
     ap.add_argument("--only-encode", action="store_true", help="headline encode loop only (for profiling)")
-    ap.add_argument("--profile-stage", choices=["prefill", "encode1", "decode1", "decode8", "decode32", "copy", "offload"],
+    ap.add_argument("--profile-stage", choices=["prefill", "encode1", "decode1", "decode8", "decode32", "copy", "offload",
+                                                "screenshot", "prefill_screenshot"],
                     help="run only this stage in a loop of --steps passes (for rocprofv3); 'copy' is a plain "
                          "1 GiB device copy that calibrates the HBM byte counters; 'offload' runs only the "
-                         "layer-offload comparison")
+                         "layer-offload comparison; 'screenshot' and 'prefill_screenshot' are the serving shapes "
+                         "(a 1092x2408 image, 13,416 patches; its 3354 visual tokens + 225 text tokens)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the method serves all three stages on a single GPU; "
-              "multi-GPU runs are not part of this build (run with --gpus 1)", file=sys.stderr)
+              "multi-GPU runs are not supported (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -722,6 +724,15 @@ def main():
 
     if args.profile_stage == "offload":
         print(json.dumps(measure_offload(nova, torch, st, ServingSetup(nova, torch, synth, st))), flush=True)
+        return
+    if args.profile_stage in ("screenshot", "prefill_screenshot"):
+        srv = ServingSetup(nova, torch, synth, st)
+        srv.encode(stream)                 # the prefill's visual tokens
+        fn = (lambda: srv.encode(stream)) if args.profile_stage == "screenshot" else (lambda: srv.prefill(stream))
+        for _ in range(args.warmup):
+            fn()
+        ms = time_passes(torch, fn, args.steps, stream)
+        log(f"{args.profile_stage}: {ms:.3f} ms per pass")
         return
     if args.profile_stage:
         fn = {"prefill": st.prefill, "encode1": lambda: st.encode(1)}.get(

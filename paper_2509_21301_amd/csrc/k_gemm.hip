@@ -653,6 +653,36 @@ static int row_split_rows(const GemmArgs& p) {
   return split <= (double)((tiles + 255) / 256) - 0.3 ? m1 * 256 : 0;
 }
 
+// 128x128 tiles with K cut into split_slices(p) slices (when that is more than one): fp32 partials
+// in p.split_ws, then summed in slice order by split_reduce_kernel (or left for the caller to fold,
+// with p.slices_out).  *done = false when the problem runs unsplit.
+template <typename OT, int EPI>
+static hipError_t launch_slices128(const GemmArgs& p, hipStream_t s, bool* done) {
+  *done = false;
+  if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
+    const int sl = p.vt == nullptr ? split_slices(p) : 1;
+    if (sl <= 1) return hipSuccess;
+    *done = true;
+    GemmArgs q = p;
+    q.out = p.split_ws;
+    q.ldo = p.N;
+    q.kslice = p.K / sl;
+    q.split_stride = (long)p.M * p.N;
+    q.vt = nullptr;
+    hipError_t e = launch_dma<float, EPI_STORE, 128, 128, 64, 64>(q, s, sl);
+    if (e != hipSuccess) return e;
+    if (EPI == EPI_RESID && p.slices_out != nullptr && p.bias == nullptr) {   // the caller folds them
+      *p.slices_out = sl;
+      return hipSuccess;
+    }
+    const long n4 = (long)p.M * (p.N / 4);
+    hipLaunchKernelGGL((split_reduce_kernel<OT, EPI>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, p,
+                       (const float*)p.split_ws, sl);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
 template <typename TA, typename OT, int EPI>
 static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
   if constexpr (sizeof(TA) == 2) {
@@ -668,6 +698,13 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
         b.A = reinterpret_cast<const bf16_t*>(p.A) + (size_t)m1 * p.lda;
         b.out = out_at<OT, EPI>(p, m1, 0);
         b.vt_row0 = p.vt_row0 + m1;
+        // the leftover rows are few tiles (a 1092x2408 screenshot's O and down projections: 30 of
+        // 128x128): with a long K they take K slices (its down projection: 4, 120 workgroups)
+        if (p.slices_out == nullptr) {
+          bool done = false;
+          const hipError_t e2 = launch_slices128<OT, EPI>(b, s, &done);
+          if (done || e2 != hipSuccess) return e2;
+        }
         return launch_dma<OT, EPI, 128, 128, 64, 64>(b, s);
       }
     }
@@ -720,25 +757,9 @@ static hipError_t launch_epi(const GemmArgs& p, hipStream_t s) {
     // tiles, 157 -> 99 us; the one-image encode's MLP up projection)
     if (p.N % 256 == 0 && tiles256 >= 192 && tiles256 < 512) return launch_dma<OT, EPI, 256, 256, 64, 128>(p, s);
     if (!(p.N % 256 == 0 && tiles256 >= 512) && p.vt == nullptr) {
-      const int sl = split_slices(p);
-      if (sl > 1) {
-        GemmArgs q = p;
-        q.out = p.split_ws;
-        q.ldo = p.N;
-        q.kslice = p.K / sl;
-        q.split_stride = (long)p.M * p.N;
-        q.vt = nullptr;
-        hipError_t e = launch_dma<float, EPI_STORE, 128, 128, 64, 64>(q, s, sl);
-        if (e != hipSuccess) return e;
-        if (EPI == EPI_RESID && p.slices_out != nullptr && p.bias == nullptr) {   // the caller folds them
-          *p.slices_out = sl;
-          return hipSuccess;
-        }
-        const long n4 = (long)p.M * (p.N / 4);
-        hipLaunchKernelGGL((split_reduce_kernel<OT, EPI>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, p,
-                           (const float*)p.split_ws, sl);
-        return hipGetLastError();
-      }
+      bool done = false;
+      const hipError_t e = launch_slices128<OT, EPI>(p, s, &done);
+      if (done || e != hipSuccess) return e;
     }
   }
   if constexpr (sizeof(TA) == 2) {

@@ -493,6 +493,8 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
     }
     {
       GemmArgs p{att, H, W(4), H, M, H, H, W(5), x, H, nullptr, 0};
+      // K-slice partials, where the GEMM takes them: the MLP hidden is free here
+      p.split_ws = reinterpret_cast<float*>(hmlp), p.split_ws_floats = (size_t)M * v->ip * sizeof(T) / sizeof(float);
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
     }
     CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, M, H, W(6), W(7), c.eps, 1, a, H, 1, 0, 0, s));
@@ -502,6 +504,8 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
     }
     {
       GemmArgs p{hmlp, v->ip, W(10), v->ip, M, H, v->ip, W(11), x, H, nullptr, 0};
+      // K-slice partials in the packed QKV buffer, free until the next layer's projection
+      p.split_ws = reinterpret_cast<float*>(qkv), p.split_ws_floats = (size_t)M * 3 * H * sizeof(T) / sizeof(float);
       CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_RESID, s)));
     }
     if (v->offload) {
@@ -521,6 +525,7 @@ int vit_encode_t(nova_vit* v, const void* pixels, int B, void* out, void* ws, hi
   CALL(NOVA_KIND_MISC, s, nova::norm_rows<T>(x, M, H, HW(0), HW(1), c.eps, 1, merged, m2 * H, c.merge, gh, gw, s));
   {
     GemmArgs p{merged, m2 * H, HW(2), m2 * H, Mo, c.out_hidden, m2 * H, HW(3), out, c.out_hidden, nullptr, 0};
+    p.split_ws = reinterpret_cast<float*>(hmlp), p.split_ws_floats = (size_t)M * v->ip * sizeof(T) / sizeof(float);
     CALL(NOVA_KIND_GEMM, s, (nova::gemm<T, T>(p, nova::EPI_STORE, s)));
   }
   return NOVA_OK;
